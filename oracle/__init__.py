@@ -1,0 +1,176 @@
+"""fp64 CPU oracle for Triangle attention and dense causal attention.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU
+baseline leg of the benchmark may import this package; the product path
+(`paper_2507_21526_amd`) never does.  The arithmetic lives in ``oracle.c``
+(plain C, double precision, OpenMP over rows) and follows the paper:
+
+* masks: the Streaming, Last Q-K and Middle Q-K sections of Appendix A.3,
+  Triangle = Streaming + Last Q-K (Sec. 2.4);
+* attention: the masked softmax of Sec. 2.1, row by row, masked logits
+  removed exactly;
+* tile schedule: brute force over every (q-tile, k-tile) block, emitted in
+  the documented packed int32 format.
+
+This module only marshals arguments through ctypes and compiles the C file
+with gcc when no built library is present.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+TRIANGLE = 0
+CAUSAL = 1
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so next to it (gcc, -O2, OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        cmd = ["gcc", "-O3", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+               "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB_PATH)
+    i64, i32, dbl = ctypes.c_int64, ctypes.c_int32, ctypes.c_double
+    vp = ctypes.c_void_p
+    lib.oracle_in_streaming.argtypes = [i64, i64, i64, i64]
+    lib.oracle_in_last.argtypes = [i64, i64, i64, i64, i64, i64]
+    lib.oracle_in_middle.argtypes = [i64, i64, i64, i64, i64, i64]
+    lib.oracle_mask.argtypes = [ctypes.c_int, i64, i64, i64, i64, i64, i64]
+    lib.oracle_mask_row.argtypes = [ctypes.c_int, i64, i64, i64, i64, i64, vp]
+    lib.oracle_mask_row.restype = None
+    lib.oracle_mask_nnz.argtypes = [ctypes.c_int, i64, i64, i64, i64]
+    lib.oracle_mask_nnz.restype = i64
+    lib.oracle_attn_rows.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32,
+                                     ctypes.c_int, i64, i64, i64, dbl,
+                                     vp, vp, i64, vp, vp]
+    lib.oracle_attn_rows.restype = ctypes.c_int
+    lib.oracle_schedule.argtypes = [ctypes.c_int, vp, i32, i32, i32, i32, i32,
+                                    i32, vp, i64]
+    lib.oracle_schedule.restype = i64
+    lib.oracle_num_threads.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _kind(kind) -> int:
+    if kind in (TRIANGLE, "triangle"):
+        return TRIANGLE
+    if kind in (CAUSAL, "causal"):
+        return CAUSAL
+    raise ValueError(f"unknown kind {kind!r}")
+
+
+def _bf16_bits(t) -> np.ndarray:
+    """Raw bf16 bit patterns of a torch bf16 tensor (or a uint16 array)."""
+    if isinstance(t, np.ndarray):
+        assert t.dtype == np.uint16
+        return np.ascontiguousarray(t)
+    import torch
+    assert t.dtype == torch.bfloat16, t.dtype
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def num_threads() -> int:
+    return int(load().oracle_num_threads())
+
+
+def in_streaming(i, j, sink, window) -> bool:
+    return bool(load().oracle_in_streaming(i, j, sink, window))
+
+
+def in_last(i, j, n, sink, window, last) -> bool:
+    return bool(load().oracle_in_last(i, j, n, sink, window, last))
+
+
+def in_middle(i, j, n, sink, window, last) -> bool:
+    return bool(load().oracle_in_middle(i, j, n, sink, window, last))
+
+
+def mask_row(kind, n, sink, window, last, i) -> np.ndarray:
+    row = np.zeros(n, dtype=np.uint8)
+    load().oracle_mask_row(_kind(kind), n, sink, window, last, i,
+                           row.ctypes.data)
+    return row
+
+
+def mask_matrix(kind, n, sink, window, last) -> np.ndarray:
+    """Full n x n mask (small n only)."""
+    return np.stack([mask_row(kind, n, sink, window, last, i) for i in range(n)]) \
+        if n > 0 else np.zeros((0, 0), np.uint8)
+
+
+def mask_nnz(kind, n, sink, window, last) -> int:
+    return int(load().oracle_mask_nnz(_kind(kind), n, sink, window, last))
+
+
+def attn_rows(q, k, v, cu_seqlens, kind, sink, window, last, scale,
+              row_tok, row_head):
+    """fp64 output rows and natural-log LSE for (token, query head) pairs.
+
+    q: [total, Hq, d], k/v: [total, Hkv, d] as torch bf16 (or uint16 bits).
+    Returns (out [nrows, d] float64, lse [nrows] float64).
+    """
+    qb, kb, vb = _bf16_bits(q), _bf16_bits(k), _bf16_bits(v)
+    total, hq, d = qb.shape
+    hkv = kb.shape[1]
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    assert cu[-1] == total and kb.shape == (total, hkv, d) and vb.shape == kb.shape
+    rt = np.ascontiguousarray(np.asarray(row_tok, dtype=np.int64))
+    rh = np.ascontiguousarray(np.asarray(row_head, dtype=np.int32))
+    assert rt.shape == rh.shape
+    out = np.zeros((rt.size, d), dtype=np.float64)
+    lse = np.zeros(rt.size, dtype=np.float64)
+    rc = load().oracle_attn_rows(qb.ctypes.data, kb.ctypes.data, vb.ctypes.data,
+                                 cu.ctypes.data, cu.size - 1, hq, hkv, d,
+                                 _kind(kind), sink, window, last, float(scale),
+                                 rt.ctypes.data, rh.ctypes.data, rt.size,
+                                 out.ctypes.data, lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_attn_rows rejected the request")
+    return out, lse
+
+
+def attn_full(q, k, v, cu_seqlens, kind, sink, window, last, scale):
+    """Every (token, head) row: returns out [total, Hq, d], lse [Hq, total]."""
+    total, hq, d = tuple(q.shape)
+    tok = np.repeat(np.arange(total, dtype=np.int64), hq)
+    head = np.tile(np.arange(hq, dtype=np.int32), total)
+    out, lse = attn_rows(q, k, v, cu_seqlens, kind, sink, window, last, scale,
+                         tok, head)
+    return out.reshape(total, hq, d), lse.reshape(total, hq).T.copy()
+
+
+def schedule(kind, cu_seqlens, sink, window, last, tile, splits=0) -> np.ndarray:
+    """Brute-force tile schedule in the packed int32 format."""
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    lib = load()
+    words = lib.oracle_schedule(_kind(kind), cu.ctypes.data, cu.size - 1, sink,
+                                window, last, tile, splits, None, 0)
+    if words < 0:
+        raise ValueError("oracle_schedule rejected the parameters")
+    out = np.zeros(words, dtype=np.int32)
+    got = lib.oracle_schedule(_kind(kind), cu.ctypes.data, cu.size - 1, sink,
+                              window, last, tile, splits, out.ctypes.data, words)
+    assert got == words
+    return out

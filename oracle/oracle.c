@@ -1,0 +1,423 @@
+/*
+ * oracle.c -- plain, slow, fp64 CPU reference for Triangle attention and
+ * dense causal attention (arXiv 2507.21526).
+ *
+ * TEST INFRASTRUCTURE ONLY: used by the tests, the smoke check and the CPU
+ * baseline of the benchmark; never by the product path.  It shares no code
+ * with the HIP library: the masks are evaluated element by element from the
+ * region definitions of Appendix A.3, attention is the masked softmax of
+ * Sec. 2.1 evaluated row by row in double precision, and the tile schedule is
+ * found by brute force over every (q-tile, k-tile) block.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+static double widen_bf16(uint16_t bits)
+{
+    uint32_t u = (uint32_t)bits << 16; /* bf16 is the top half of an fp32 */
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* ---- Appendix A.3: the three sections of the causal attention matrix ---- */
+
+/* Streaming section: the sink keys and the sliding window, causal. */
+int oracle_in_streaming(int64_t i, int64_t j, int64_t sink, int64_t window)
+{
+    if (!(i >= j))
+        return 0;
+    return (j < sink) || (i - j < window);
+}
+
+static int64_t last_rows(int64_t n, int64_t last)
+{
+    return last < n ? last : n;
+}
+
+/* Last Q-K section: the last rows, outside the streaming section, causal. */
+int oracle_in_last(int64_t i, int64_t j, int64_t n, int64_t sink,
+                   int64_t window, int64_t last)
+{
+    if (!(i >= j))
+        return 0;
+    if (!(i >= n - last_rows(n, last)))
+        return 0;
+    return (j >= sink) && (i - j >= window);
+}
+
+/* Middle Q-K section: what Triangle attention skips. */
+int oracle_in_middle(int64_t i, int64_t j, int64_t n, int64_t sink,
+                     int64_t window, int64_t last)
+{
+    if (!(i >= j))
+        return 0;
+    if (!(i < n - last_rows(n, last)))
+        return 0;
+    return (j >= sink) && (i - j >= window);
+}
+
+/* Sec. 2.4: Triangle = Streaming section plus Last Q-K section. */
+int oracle_mask(int kind, int64_t i, int64_t j, int64_t n, int64_t sink,
+                int64_t window, int64_t last)
+{
+    if (kind == ORACLE_CAUSAL)
+        return i >= j;
+    return oracle_in_streaming(i, j, sink, window) ||
+           oracle_in_last(i, j, n, sink, window, last);
+}
+
+void oracle_mask_row(int kind, int64_t n, int64_t sink, int64_t window,
+                     int64_t last, int64_t i, uint8_t *row)
+{
+    for (int64_t j = 0; j < n; ++j)
+        row[j] = (uint8_t)oracle_mask(kind, i, j, n, sink, window, last);
+}
+
+int64_t oracle_mask_nnz(int kind, int64_t n, int64_t sink, int64_t window,
+                        int64_t last)
+{
+    int64_t total = 0;
+#pragma omp parallel for reduction(+ : total) schedule(dynamic, 64)
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < n; ++j)
+            total += oracle_mask(kind, i, j, n, sink, window, last);
+    return total;
+}
+
+/* ---- Sec. 2.1: masked softmax attention, one (row, head) at a time ---- */
+
+int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                     const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                     int32_t hkv, int32_t d, int kind, int64_t sink,
+                     int64_t window, int64_t last, double scale,
+                     const int64_t *row_tok, const int32_t *row_head,
+                     int64_t nrows, double *out, double *lse)
+{
+    if (batch < 0 || hq <= 0 || hkv <= 0 || d <= 0 || hq % hkv != 0)
+        return -1;
+    const int64_t total = cu_seqlens[batch];
+    const int32_t group = hq / hkv;
+    for (int64_t r = 0; r < nrows; ++r) {
+        if (row_tok[r] < 0 || row_tok[r] >= total || row_head[r] < 0 ||
+            row_head[r] >= hq)
+            return -1;
+    }
+
+    int bad = 0;
+#pragma omp parallel
+    {
+        int64_t cap = 0;
+        uint8_t *mask = NULL;
+        double *z = NULL;
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < nrows; ++r) {
+            const int64_t t = row_tok[r];
+            const int32_t h = row_head[r];
+            const int32_t g = h / group;
+            int32_t b = 0;
+            while (!(cu_seqlens[b] <= t && t < cu_seqlens[b + 1]))
+                ++b;
+            const int64_t off = cu_seqlens[b];
+            const int64_t n = cu_seqlens[b + 1] - off;
+            const int64_t i = t - off;
+            if (n > cap) {
+                free(mask);
+                free(z);
+                cap = n;
+                mask = (uint8_t *)malloc((size_t)n);
+                z = (double *)malloc((size_t)n * sizeof(double));
+            }
+            if (!mask || !z) {
+#pragma omp atomic write
+                bad = 1;
+                continue;
+            }
+            oracle_mask_row(kind, n, sink, window, last, i, mask);
+
+            const uint16_t *qi = q + ((size_t)t * hq + h) * d;
+            double zmax = -INFINITY;
+            for (int64_t j = 0; j < n; ++j) {
+                if (!mask[j])
+                    continue;
+                const uint16_t *kj = k + ((size_t)(off + j) * hkv + g) * d;
+                double dot = 0.0;
+                for (int32_t c = 0; c < d; ++c)
+                    dot += widen_bf16(qi[c]) * widen_bf16(kj[c]);
+                z[j] = scale * dot;
+                if (z[j] > zmax)
+                    zmax = z[j];
+            }
+            double *o = out + (size_t)r * d;
+            for (int32_t c = 0; c < d; ++c)
+                o[c] = 0.0;
+            double denom = 0.0;
+            for (int64_t j = 0; j < n; ++j) {
+                if (!mask[j])
+                    continue;
+                const double p = exp(z[j] - zmax);
+                denom += p;
+                const uint16_t *vj = v + ((size_t)(off + j) * hkv + g) * d;
+                for (int32_t c = 0; c < d; ++c)
+                    o[c] += p * widen_bf16(vj[c]);
+            }
+            for (int32_t c = 0; c < d; ++c)
+                o[c] /= denom;
+            if (lse)
+                lse[r] = zmax + log(denom);
+        }
+        free(mask);
+        free(z);
+    }
+    return bad ? -1 : 0;
+}
+
+/* ---- Tile schedule by brute force over blocks ----
+ *
+ * Packed int32 format (documented with the library's interface):
+ *   header, 16 words: magic, version, kind, tile, batch, sink, window, last,
+ *     splits requested, total_tokens (low, high 32 bits), main items, merge
+ *     items, partial rows, kept k-tiles per query head, 0.
+ *   main item, 12 words: seq_off, seq_len, r0, r1, ka0, ka1, kb0, kb1, mode,
+ *     part_base, kept k-tiles, 0.   Rows [r0, r1) are relative to the
+ *     sequence start; [ka0, ka1) and [kb0, kb1) are the kept k-tiles as at
+ *     most two maximal runs in increasing order (an absent run is (0, 0));
+ *     mode 0 = streaming mask, 1 = causal mask; part_base -1 = the item
+ *     writes the output rows, else it writes partial rows part_base + (i - r0).
+ *   merge item, 8 words: seq_off, r0, r1, splits, part_base, 0, 0, 0.
+ * Triangle order: the Last split items (by sequence, q-tile, split), then the
+ * streaming items (by sequence, q-tile).  Causal order: by kept k-tiles,
+ * descending, ties in (sequence, q-tile) order.
+ */
+
+enum { HDR_WORDS = 16, ITEM_WORDS = 12, MERGE_WORDS = 8 };
+static const int32_t SCHED_MAGIC = 0x54524941;
+static const int32_t SCHED_VERSION = 1;
+
+typedef struct {
+    int32_t w[ITEM_WORDS];
+} item_t;
+
+typedef struct {
+    item_t *v;
+    int64_t n, cap;
+} item_vec;
+
+static int push_item(item_vec *iv, const item_t *it)
+{
+    if (iv->n == iv->cap) {
+        int64_t nc = iv->cap ? 2 * iv->cap : 256;
+        item_t *nv = (item_t *)realloc(iv->v, (size_t)nc * sizeof(item_t));
+        if (!nv)
+            return -1;
+        iv->v = nv;
+        iv->cap = nc;
+    }
+    iv->v[iv->n++] = *it;
+    return 0;
+}
+
+/* kept[qt * nkt + kt] = 1 iff block (q-tile qt, k-tile kt) holds a kept pair.
+ * q-tile qt covers rows [row0 + qt*tile, min(row0 + (qt+1)*tile, row1)). */
+static void kept_blocks(int kind, int64_t n, int64_t sink, int64_t window,
+                        int64_t last, int64_t tile, int64_t row0,
+                        int64_t row1, int64_t nqt, int64_t nkt, uint8_t *kept)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t qt = 0; qt < nqt; ++qt) {
+        const int64_t r0 = row0 + qt * tile;
+        const int64_t r1 = (r0 + tile < row1) ? r0 + tile : row1;
+        for (int64_t kt = 0; kt < nkt; ++kt) {
+            const int64_t c0 = kt * tile;
+            const int64_t c1 = (c0 + tile < n) ? c0 + tile : n;
+            int any = 0;
+            for (int64_t i = r0; i < r1 && !any; ++i)
+                for (int64_t j = c0; j < c1; ++j)
+                    any |= oracle_mask(kind, i, j, n, sink, window, last);
+            kept[qt * nkt + kt] = (uint8_t)(any != 0);
+        }
+    }
+}
+
+/* Split maximal runs of kept k-tiles; returns the number of runs (<= 2 kept). */
+static int runs_of(const uint8_t *kept, int64_t nkt, int64_t run[2][2])
+{
+    int nruns = 0;
+    run[0][0] = run[0][1] = run[1][0] = run[1][1] = 0;
+    for (int64_t kt = 0; kt < nkt;) {
+        if (!kept[kt]) {
+            ++kt;
+            continue;
+        }
+        int64_t e = kt;
+        while (e < nkt && kept[e])
+            ++e;
+        if (nruns >= 2)
+            return 3;
+        run[nruns][0] = kt;
+        run[nruns][1] = e;
+        ++nruns;
+        kt = e;
+    }
+    return nruns;
+}
+
+int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
+                        int32_t sink, int32_t window, int32_t last,
+                        int32_t tile, int32_t splits, int32_t *out,
+                        int64_t cap)
+{
+    if ((kind != ORACLE_TRIANGLE && kind != ORACLE_CAUSAL) || batch < 0 ||
+        tile < 1 || sink < 0 || window < 1 || last < 0 || splits < 0 ||
+        cu_seqlens[0] != 0)
+        return -1;
+    for (int32_t b = 0; b < batch; ++b)
+        if (cu_seqlens[b + 1] < cu_seqlens[b])
+            return -1;
+
+    item_vec last_items = {0}, main_items = {0}, merges = {0};
+    int64_t partial_rows = 0, kept_total = 0;
+    int fail = 0;
+    /* steady-state streaming work of one q-tile, in k-tiles */
+    const int64_t t_star = (sink + tile - 1) / tile +
+                           (window + tile - 1) / tile + 1;
+
+    for (int32_t b = 0; b < batch && !fail; ++b) {
+        const int64_t off = cu_seqlens[b];
+        const int64_t n = cu_seqlens[b + 1] - off;
+        if (n == 0)
+            continue;
+        const int64_t nkt = (n + tile - 1) / tile;
+        const int64_t lr = (kind == ORACLE_TRIANGLE) ? last_rows(n, last) : 0;
+        /* region 0: rows [0, n - lr) ; region 1 (Triangle only): [n - lr, n) */
+        for (int region = 0; region < 2 && !fail; ++region) {
+            const int64_t row0 = region == 0 ? 0 : n - lr;
+            const int64_t row1 = region == 0 ? n - lr : n;
+            if (row1 <= row0)
+                continue;
+            const int64_t nqt = (row1 - row0 + tile - 1) / tile;
+            uint8_t *kept = (uint8_t *)malloc((size_t)(nqt * nkt));
+            if (!kept) {
+                fail = 1;
+                break;
+            }
+            kept_blocks(kind, n, sink, window, last, tile, row0, row1, nqt,
+                        nkt, kept);
+            for (int64_t qt = 0; qt < nqt && !fail; ++qt) {
+                const int64_t r0 = row0 + qt * tile;
+                const int64_t r1 = (r0 + tile < row1) ? r0 + tile : row1;
+                int64_t run[2][2];
+                const int nr = runs_of(kept + qt * nkt, nkt, run);
+                if (nr < 1 || nr > 2) {
+                    fail = 1;
+                    break;
+                }
+                const int64_t cost = (run[0][1] - run[0][0]) +
+                                     (run[1][1] - run[1][0]);
+                kept_total += cost;
+                if (region == 0) {
+                    item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0,
+                                  (int32_t)r1, (int32_t)run[0][0],
+                                  (int32_t)run[0][1], (int32_t)run[1][0],
+                                  (int32_t)run[1][1],
+                                  kind == ORACLE_CAUSAL ? 1 : 0, -1,
+                                  (int32_t)cost, 0}};
+                    fail |= push_item(&main_items, &it);
+                    continue;
+                }
+                /* Last q-tile: every k-tile up to the diagonal, cut into
+                 * balanced contiguous splits (Appendix A.1, Alg. 1). */
+                if (nr != 1 || run[0][0] != 0) {
+                    fail = 1;
+                    break;
+                }
+                const int64_t nk = run[0][1];
+                int64_t ns = splits > 0 ? splits : (nk + t_star - 1) / t_star;
+                if (ns < 1)
+                    ns = 1;
+                if (ns > nk)
+                    ns = nk;
+                for (int64_t c = 0; c < ns; ++c) {
+                    const int64_t k0 = c * nk / ns, k1 = (c + 1) * nk / ns;
+                    item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0,
+                                  (int32_t)r1, (int32_t)k0, (int32_t)k1, 0, 0,
+                                  1, (int32_t)(partial_rows + c * (r1 - r0)),
+                                  (int32_t)(k1 - k0), 0}};
+                    fail |= push_item(&last_items, &it);
+                }
+                item_t m = {{(int32_t)off, (int32_t)r0, (int32_t)r1,
+                             (int32_t)ns, (int32_t)partial_rows, 0, 0, 0, 0,
+                             0, 0, 0}};
+                fail |= push_item(&merges, &m);
+                partial_rows += ns * (r1 - r0);
+            }
+            free(kept);
+        }
+    }
+
+    if (!fail && kind == ORACLE_CAUSAL) {
+        /* stable ordering by kept k-tiles, descending (insertion sort keeps
+         * equal costs in their (sequence, q-tile) order) */
+        for (int64_t a = 1; a < main_items.n; ++a) {
+            item_t x = main_items.v[a];
+            int64_t p = a - 1;
+            while (p >= 0 && main_items.v[p].w[10] < x.w[10]) {
+                main_items.v[p + 1] = main_items.v[p];
+                --p;
+            }
+            main_items.v[p + 1] = x;
+        }
+    }
+
+    int64_t words = -1;
+    if (!fail) {
+        const int64_t n_main = last_items.n + main_items.n;
+        words = HDR_WORDS + n_main * ITEM_WORDS + merges.n * MERGE_WORDS;
+        if (out && cap >= words) {
+            const int64_t total = cu_seqlens[batch];
+            int32_t *w = out;
+            w[0] = SCHED_MAGIC;
+            w[1] = SCHED_VERSION;
+            w[2] = kind;
+            w[3] = tile;
+            w[4] = batch;
+            w[5] = sink;
+            w[6] = window;
+            w[7] = last;
+            w[8] = splits;
+            w[9] = (int32_t)(uint32_t)((uint64_t)total & 0xffffffffu);
+            w[10] = (int32_t)(uint32_t)((uint64_t)total >> 32);
+            w[11] = (int32_t)n_main;
+            w[12] = (int32_t)merges.n;
+            w[13] = (int32_t)partial_rows;
+            w[14] = (int32_t)kept_total;
+            w[15] = 0;
+            w += HDR_WORDS;
+            for (int64_t a = 0; a < last_items.n; ++a, w += ITEM_WORDS)
+                memcpy(w, last_items.v[a].w, sizeof(int32_t) * ITEM_WORDS);
+            for (int64_t a = 0; a < main_items.n; ++a, w += ITEM_WORDS)
+                memcpy(w, main_items.v[a].w, sizeof(int32_t) * ITEM_WORDS);
+            for (int64_t a = 0; a < merges.n; ++a, w += MERGE_WORDS)
+                memcpy(w, merges.v[a].w, sizeof(int32_t) * MERGE_WORDS);
+        }
+    }
+    free(last_items.v);
+    free(main_items.v);
+    free(merges.v);
+    return words;
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,114 @@
+"""Seeded synthetic inputs and the workload table.
+
+This module holds no attention arithmetic: it draws the Q/K/V tensors that
+both the HIP path and the CPU oracle consume, so that the two sides read the
+same bf16 bytes.  Values are drawn in fp32 from a seeded CPU
+``torch.Generator`` (i.i.d. N(0, 1), optionally scaled per head or with a
+boosted key 0) and rounded once to bf16 (round to nearest even).
+
+The workloads stand in for the attention-kernel latency measurements of the
+paper (Sec. 3.4, table of attention kernel latency: Llama-3.1-8B and
+Qwen2.5-7B attention layers at 32K to 128K tokens); the shapes are those
+models' attention shapes, the values are synthetic.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import torch
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    cu_seqlens: tuple
+    hq: int
+    hkv: int
+    d: int
+    tile: int
+    sink: int
+    window: int
+    last: int
+    seed: int
+    head_scale: tuple | None = None      # (lo, hi): per-(tensor, head) U[lo, hi]
+    key0_boost: float | None = None      # multiply K[0, :, :] by this factor
+    layers: int = 1
+    triangle_layers: int = 1             # how many of the layers use Triangle
+    note: str = ""
+
+    @property
+    def total(self) -> int:
+        return int(self.cu_seqlens[-1])
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.d)
+
+
+WORKLOADS = {
+    "tiny_n1024_d64": Workload(
+        "tiny_n1024_d64", (0, 1024), hq=4, hkv=1, d=64, tile=64, sink=64,
+        window=256, last=64, seed=1001,
+        note="one layer, GQA 4:1, N=1024, d=64"),
+    "llama8b_n32k": Workload(
+        "llama8b_n32k", (0, 32768), hq=32, hkv=8, d=128, tile=128, sink=128,
+        window=2048, last=128, seed=1002, head_scale=(0.5, 2.0),
+        note="Llama-3.1-8B attention shape, N=32768, per-head RMS scale"),
+    "llama8b_n128k": Workload(
+        "llama8b_n128k", (0, 131072), hq=32, hkv=8, d=128, tile=128, sink=128,
+        window=2048, last=128, seed=1003, key0_boost=8.0,
+        note="Llama-3.1-8B attention shape, N=131072, key 0 with 8x norm"),
+    "llama8b_varlen4": Workload(
+        "llama8b_varlen4", (0, 8192, 32768, 81920, 147456), hq=32, hkv=8,
+        d=128, tile=128, sink=128, window=2048, last=128, seed=1004,
+        note="4 packed sequences of 8K, 24K, 48K, 64K tokens"),
+    "qwen7b_n128k_stack28": Workload(
+        "qwen7b_n128k_stack28", (0, 131072), hq=28, hkv=4, d=128, tile=128,
+        sink=128, window=4096, last=256, seed=1005, layers=28,
+        triangle_layers=20,
+        note="Qwen2.5-7B attention shape, 28 layers: 20 Triangle, 8 dense"),
+}
+
+
+def draw_qkv(cu_seqlens, hq: int, hkv: int, d: int, seed: int,
+             head_scale=None, key0_boost=None):
+    """Seeded bf16 Q [T, Hq, d], K and V [T, Hkv, d] on the CPU.
+
+    Draw order from one generator: Q, K, V (N(0, 1) fp32), then, if
+    ``head_scale`` is given, per-head factors U[lo, hi] for Q (Hq values),
+    K and V (Hkv values each).  ``key0_boost`` multiplies the key of token 0
+    of every kv head.  A single rounding to bf16 ends the draw.
+    """
+    total = int(cu_seqlens[-1])
+    gen = torch.Generator(device="cpu").manual_seed(int(seed))
+    q = torch.randn((total, hq, d), generator=gen, dtype=torch.float32)
+    k = torch.randn((total, hkv, d), generator=gen, dtype=torch.float32)
+    v = torch.randn((total, hkv, d), generator=gen, dtype=torch.float32)
+    if head_scale is not None:
+        lo, hi = head_scale
+        sq = lo + (hi - lo) * torch.rand(hq, generator=gen, dtype=torch.float32)
+        sk = lo + (hi - lo) * torch.rand(hkv, generator=gen, dtype=torch.float32)
+        sv = lo + (hi - lo) * torch.rand(hkv, generator=gen, dtype=torch.float32)
+        q.mul_(sq.view(1, hq, 1))
+        k.mul_(sk.view(1, hkv, 1))
+        v.mul_(sv.view(1, hkv, 1))
+    if key0_boost is not None and total > 0:
+        k[0].mul_(float(key0_boost))
+    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+
+
+def workload_qkv(w: Workload, layer: int = 0):
+    """Inputs of one layer of a workload (layer l of a stack: seed*1000 + l)."""
+    seed = w.seed if w.layers == 1 else w.seed * 1000 + layer
+    return draw_qkv(w.cu_seqlens, w.hq, w.hkv, w.d, seed, w.head_scale,
+                    w.key0_boost)
+
+
+def triangle_layer_set(w: Workload) -> list:
+    """Seeded choice of which layers of a stack use Triangle attention."""
+    if w.layers == 1:
+        return [0]
+    gen = torch.Generator(device="cpu").manual_seed(int(w.seed))
+    perm = torch.randperm(w.layers, generator=gen)
+    return sorted(int(x) for x in perm[: w.triangle_layers])

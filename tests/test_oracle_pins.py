@@ -1,0 +1,268 @@
+"""Pins of the fp64 oracle against things other than itself.
+
+Each test fixes the oracle to something the paper or mathematics determines:
+hand-drawn masks (tests/golden), the partition of the causal matrix into the
+three sections of Appendix A.3, library attention (torch SDPA in float64),
+textbook softmax on tiny inputs, closed-form counts, and the invariants that
+follow from the definitions (Triangle equals causal exactly when the Middle
+Q-K section is empty; the Last rows are causal rows; row 0 sees only key 0).
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2507_21526_amd.inputs import draw_qkv
+from tests.conftest import read_mask_fixture
+
+
+# ---------------------------------------------------------------- masks ----
+
+def test_golden_triangle_mask(golden_dir):
+    want = read_mask_fixture(os.path.join(golden_dir,
+                                          "triangle_mask_n10_s2_w3_l2.txt"))
+    got = oracle.mask_matrix("triangle", 10, 2, 3, 2)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_golden_streaming_mask(golden_dir):
+    want = read_mask_fixture(os.path.join(golden_dir,
+                                          "streaming_mask_n9_s1_w2_l0.txt"))
+    got = oracle.mask_matrix("triangle", 9, 1, 2, 0)
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("n,S,W,L", [(1, 0, 1, 0), (7, 2, 3, 1), (12, 3, 4, 5),
+                                     (16, 0, 1, 16), (20, 5, 2, 0),
+                                     (33, 4, 8, 7)])
+def test_sections_partition_causal(n, S, W, L):
+    """Streaming, Last Q-K and Middle Q-K are disjoint and cover j <= i."""
+    for i in range(n):
+        for j in range(n):
+            s = oracle.in_streaming(i, j, S, W)
+            l_ = oracle.in_last(i, j, n, S, W, L)
+            m = oracle.in_middle(i, j, n, S, W, L)
+            assert s + l_ + m == (1 if j <= i else 0), (i, j)
+            tri = oracle.mask_row("triangle", n, S, W, L, i)[j]
+            assert tri == (1 if (s or l_) else 0)
+            assert oracle.mask_row("causal", n, S, W, L, i)[j] == (j <= i)
+
+
+def _nnz_closed_form(n, S, W, L):
+    """Count by rows: a streaming row i keeps min(i+1, W) window keys plus the
+    sink keys left of the window; a Last row keeps all i+1 keys."""
+    lr = min(L, n)
+    total = 0
+    for i in range(n - lr):
+        total += min(i + 1, W) + min(S, max(0, i - W + 1))
+    for i in range(n - lr, n):
+        total += i + 1
+    return total
+
+
+@pytest.mark.parametrize("n,S,W,L", [(1, 0, 1, 0), (50, 3, 7, 5), (64, 64, 1, 0),
+                                     (100, 0, 100, 3), (257, 16, 31, 9),
+                                     (1024, 64, 256, 64)])
+def test_nnz_closed_form(n, S, W, L):
+    assert oracle.mask_nnz("triangle", n, S, W, L) == _nnz_closed_form(n, S, W, L)
+    assert oracle.mask_nnz("causal", n, S, W, L) == n * (n + 1) // 2
+
+
+def test_nnz_published_counts():
+    # Per-head kept-pair counts of the tiny and 32K workloads.
+    assert oracle.mask_nnz("triangle", 1024, 64, 256, 64) == 319680
+    assert oracle.mask_nnz("triangle", 32768, 128, 2048, 128) == 72844416
+
+
+@pytest.mark.parametrize("S,W,L", [(0, 1, 0), (1, 1, 1), (2, 3, 0), (3, 2, 4),
+                                   (4, 5, 2), (0, 4, 3)])
+def test_triangle_equals_causal_iff_middle_empty(S, W, L):
+    """Middle Q-K is empty iff n <= S + W + L; at n = S+W+L+1 exactly the pair
+    (row S+W, key S) is dropped."""
+    for n in range(1, S + W + L + 4):
+        tri = oracle.mask_matrix("triangle", n, S, W, L)
+        cau = oracle.mask_matrix("causal", n, S, W, L)
+        diff = np.argwhere(tri != cau)
+        if n <= S + W + L:
+            assert diff.size == 0, n
+        if n == S + W + L + 1:
+            assert diff.tolist() == [[S + W, S]]
+        assert np.all(tri <= cau)
+
+
+# ------------------------------------------------------------ attention ----
+
+def _sdpa_ref(q, k, v, cu, kind, S, W, L, scale):
+    """torch SDPA in float64 on the CPU, per sequence, with an explicit bool
+    mask and K/V expanded to the query heads by repeat_interleave."""
+    hq, hkv = q.shape[1], k.shape[1]
+    g = hq // hkv
+    outs = []
+    for b in range(len(cu) - 1):
+        s, e = cu[b], cu[b + 1]
+        n = e - s
+        if n == 0:
+            continue
+        m = torch.from_numpy(oracle.mask_matrix(kind, n, S, W, L)).bool()
+        qd = q[s:e].double().transpose(0, 1)
+        kd = k[s:e].double().repeat_interleave(g, dim=1).transpose(0, 1)
+        vd = v[s:e].double().repeat_interleave(g, dim=1).transpose(0, 1)
+        o = torch.nn.functional.scaled_dot_product_attention(
+            qd, kd, vd, attn_mask=m, scale=scale)
+        outs.append(o.transpose(0, 1))
+    return torch.cat(outs, 0).numpy()
+
+
+@pytest.mark.parametrize("kind", ["triangle", "causal"])
+@pytest.mark.parametrize("cu,hq,hkv,d,S,W,L", [
+    ([0, 200], 4, 1, 64, 16, 32, 8),
+    ([0, 130], 2, 2, 128, 0, 7, 0),
+    ([0, 37, 37, 300, 512], 6, 2, 64, 5, 40, 20),
+    ([0, 96], 7, 1, 128, 8, 16, 100),
+])
+def test_oracle_matches_sdpa_fp64(kind, cu, hq, hkv, d, S, W, L):
+    q, k, v = draw_qkv(cu, hq, hkv, d, seed=11 + d + hq)
+    scale = 1.0 / math.sqrt(d)
+    out, _ = oracle.attn_full(q, k, v, cu, kind, S, W, L, scale)
+    ref = _sdpa_ref(q, k, v, cu, kind, S, W, L, scale)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_oracle_matches_textbook_softmax():
+    """exp / sum without the max shift, on small logits, in numpy fp64."""
+    cu = [0, 40]
+    q, k, v = draw_qkv(cu, 2, 1, 64, seed=5)
+    S, W, L, scale = 3, 6, 4, 0.05
+    out, lse = oracle.attn_full(q, k, v, cu, "triangle", S, W, L, scale)
+    qd, kd, vd = (x.double().numpy() for x in (q, k, v))
+    mask = oracle.mask_matrix("triangle", 40, S, W, L)
+    for h in range(2):
+        for i in range(40):
+            num = np.zeros(64)
+            den = 0.0
+            for j in range(40):
+                if mask[i, j]:
+                    e = math.exp(scale * float(qd[i, h] @ kd[j, 0]))
+                    num += e * vd[j, 0]
+                    den += e
+            np.testing.assert_allclose(out[i, h], num / den, rtol=1e-12,
+                                       atol=1e-13)
+            assert abs(lse[h, i] - math.log(den)) < 1e-12
+
+
+def test_last_rows_equal_causal_rows():
+    cu = [0, 300]
+    S, W, L = 4, 16, 37
+    q, k, v = draw_qkv(cu, 4, 2, 64, seed=9)
+    tri, tl = oracle.attn_full(q, k, v, cu, "triangle", S, W, L, 0.125)
+    cau, cl = oracle.attn_full(q, k, v, cu, "causal", S, W, L, 0.125)
+    np.testing.assert_array_equal(tri[300 - L:], cau[300 - L:])
+    np.testing.assert_array_equal(tl[:, 300 - L:], cl[:, 300 - L:])
+    # rows inside the first S + W are also causal rows
+    np.testing.assert_array_equal(tri[:S + W], cau[:S + W])
+    # and a middle row differs
+    assert np.abs(tri[S + W + 10] - cau[S + W + 10]).max() > 1e-6
+
+
+def test_row0_sees_only_key0():
+    cu = [0, 64, 100]
+    q, k, v = draw_qkv(cu, 2, 1, 64, seed=3)
+    out, lse = oracle.attn_full(q, k, v, cu, "triangle", 2, 8, 4, 0.3)
+    for s in (0, 64):
+        for h in range(2):
+            np.testing.assert_array_equal(out[s, h], v[s, 0].double().numpy())
+            want = 0.3 * float(q[s, h].double() @ k[s, 0].double())
+            assert abs(lse[h, s] - want) < 1e-12
+
+
+def test_streaming_with_full_window_is_causal():
+    cu = [0, 80]
+    q, k, v = draw_qkv(cu, 2, 2, 64, seed=4)
+    a, _ = oracle.attn_full(q, k, v, cu, "triangle", 0, 80, 0, 0.125)
+    b, _ = oracle.attn_full(q, k, v, cu, "causal", 0, 0, 0, 0.125)
+    np.testing.assert_array_equal(a, b)
+
+
+def test_packed_sequences_do_not_interact():
+    cu = [0, 50, 130]
+    q, k, v = draw_qkv(cu, 2, 1, 64, seed=8)
+    packed, _ = oracle.attn_full(q, k, v, cu, "triangle", 2, 9, 5, 0.125)
+    for s, e in ((0, 50), (50, 130)):
+        alone, _ = oracle.attn_full(q[s:e], k[s:e], v[s:e], [0, e - s],
+                                    "triangle", 2, 9, 5, 0.125)
+        np.testing.assert_array_equal(packed[s:e], alone)
+
+
+# --------------------------------------------------------- tile schedule ----
+
+HDR, ITEM, MERGE = 16, 12, 8
+
+
+def _items(words):
+    n_main, n_merge = words[11], words[12]
+    main = words[HDR:HDR + n_main * ITEM].reshape(n_main, ITEM)
+    merge = words[HDR + n_main * ITEM:].reshape(n_merge, MERGE)
+    return main, merge
+
+
+@pytest.mark.parametrize("kind", ["triangle", "causal"])
+@pytest.mark.parametrize("cu,S,W,L,T", [
+    ([0, 1024], 64, 256, 64, 64),
+    ([0, 1000], 8, 100, 50, 64),
+    ([0, 130, 130, 700], 0, 1, 3, 64),
+    ([0, 333], 40, 70, 0, 32),
+    ([0, 64, 200, 201], 5, 500, 1000, 16),
+])
+def test_schedule_minimal_and_complete(kind, cu, S, W, L, T):
+    """Independent numpy check of the brute-force schedule: the kept tiles of
+    every q-tile are exactly the blocks of the full mask that hold a 1; every
+    Last row is covered by its splits once."""
+    words = oracle.schedule(kind, cu, S, W, L, T)
+    main, merge = _items(words)
+    seen = {}
+    for it in main:
+        off, n, r0, r1, ka0, ka1, kb0, kb1, mode, pb, cost, _ = it.tolist()
+        tiles = list(range(ka0, ka1)) + list(range(kb0, kb1))
+        assert cost == len(tiles)
+        seen.setdefault((off, r0, r1), []).extend(tiles)
+    for b in range(len(cu) - 1):
+        off, n = cu[b], cu[b + 1] - cu[b]
+        if n == 0:
+            continue
+        m = oracle.mask_matrix(kind, n, S, W, L)
+        lr = min(L, n) if kind == "triangle" else 0
+        regions = [(0, n - lr), (n - lr, n)]
+        nkt = -(-n // T)
+        for r_lo, r_hi in regions:
+            for r0 in range(r_lo, r_hi, T):
+                r1 = min(r0 + T, r_hi)
+                want = [kt for kt in range(nkt)
+                        if m[r0:r1, kt * T:min(kt * T + T, n)].any()]
+                got = sorted(seen.pop((off, r0, r1)))
+                assert got == want, (off, r0, r1)
+    assert not seen
+    assert words[14] == sum(int(x) for x in main[:, 10])
+
+
+def test_schedule_published_kept_tiles():
+    # Kept k-tiles per query head (streaming + Last) of the tiny, 32K and
+    # varlen workloads, and of dense causal at 32K.
+    assert oracle.schedule("triangle", [0, 1024], 64, 256, 64, 64)[14] == 91
+    assert oracle.schedule("causal", [0, 1024], 64, 256, 64, 64)[14] == 136
+    assert oracle.schedule("triangle", [0, 32768], 128, 2048, 128, 128)[14] == 4693
+    assert oracle.schedule("causal", [0, 32768], 128, 2048, 128, 128)[14] == 32896
+
+
+def test_schedule_splits_balanced():
+    words = oracle.schedule("triangle", [0, 4096], 64, 256, 64, 64, splits=7)
+    main, merge = _items(words)
+    last = main[main[:, 9] >= 0]
+    assert len(merge) == 1 and merge[0, 3] == 7
+    ranges = [(int(a), int(b)) for a, b in last[:, 4:6]]
+    assert ranges[0][0] == 0 and ranges[-1][1] == 64
+    assert all(ranges[c][1] == ranges[c + 1][0] for c in range(6))
+    sizes = [b - a for a, b in ranges]
+    assert max(sizes) - min(sizes) <= 1
