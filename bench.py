@@ -1,0 +1,295 @@
+#!/usr/bin/env python3
+"""Triangle attention prefill benchmark on one MI355X.
+
+One step = one Triangle attention forward (the streaming and Last-row split
+pass, then the merge of the split partials) over the Llama-3.1-8B-shaped
+128K-token layer: Q [131072, 32, 128], K/V [131072, 8, 128], bf16, S=128,
+W=2048, L=128, tile 128.  Inputs and the schedule are resident in HBM before
+timing starts (the schedule is built once per (cu_seqlens, S, W, L, tile)
+on the host; its build time is reported separately).  The dense causal
+forward on the same inputs is timed with the same protocol for the speedup.
+
+Prints ONE JSON line on stdout (logs go to stderr):
+  value     = kept-tile FLOPs / ms_per_step, in TFLOP/s (kept-tile FLOPs =
+              kept (q-tile, k-tile) pairs x Hq x 4 T^2 d)
+  roofline  = the tile kernel (dominant): kept-tile FLOPs per launch over its
+              mean launch time from HIP events on the launch stream, against
+              the bf16 dense MFMA peak of MI355X (2.5 PFLOP/s)
+  cpu_baseline = the fp64 oracle on the host cores, timed on a bounded row
+              sample of the same workload and extrapolated per row class.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PAPER_SPEEDUP_128K = 15.3   # Triangle vs FlashAttention, A100 80GB, Sec. 3.4
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in ("paper_2507_21526_amd/csrc/triattn_fwd.hip",
+                "paper_2507_21526_amd/csrc/triattn_internal.h"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM bytes per tile-kernel launch from committed rocprofv3 counter runs,
+    or None when absent or taken on another version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_tile_kernel_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, q, k, v, target_s: float, kept_flops: float):
+    """Time the fp64 oracle on a bounded sample of rows of the workload and
+    extrapolate to the whole pass per row class (streaming rows, Last rows)."""
+    import numpy as np
+    import oracle
+
+    rng = np.random.default_rng(w.seed)
+    cu = list(w.cu_seqlens)
+    stream_rows, last_rows = [], []
+    for b in range(len(cu) - 1):
+        off, n = cu[b], cu[b + 1] - cu[b]
+        lr = min(w.last, n)
+        stream_rows.extend(range(off, off + n - lr))
+        last_rows.extend(range(off + n - lr, off + n))
+    stream_rows = np.array(stream_rows, dtype=np.int64)
+    last_rows = np.array(last_rows, dtype=np.int64)
+
+    def timed(rows, count):
+        tok = rng.choice(rows, size=count, replace=True)
+        head = rng.integers(0, w.hq, size=count).astype(np.int32)
+        t0 = time.perf_counter()
+        oracle.attn_rows(q, k, v, cu, "triangle", w.sink, w.window, w.last,
+                         w.scale, tok, head)
+        return (time.perf_counter() - t0) / count
+
+    # calibrate, then size the sample to about target_s seconds in total
+    t_s = timed(stream_rows, 64)
+    t_l = timed(last_rows, 8) if last_rows.size else 0.0
+    n_s = max(64, int(0.5 * target_s / max(t_s, 1e-6)))
+    n_l = max(8, int(0.5 * target_s / max(t_l, 1e-6))) if last_rows.size else 0
+    t0 = time.perf_counter()
+    t_s = timed(stream_rows, n_s)
+    t_l = timed(last_rows, n_l) if n_l else 0.0
+    spent = time.perf_counter() - t0
+    full_s = (stream_rows.size * t_s + last_rows.size * t_l) * w.hq
+    return {
+        "value": kept_flops / full_s / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"{n_s} streaming and {n_l} Last (row, head) pairs of "
+                   f"{w.name} Triangle attention in fp64 ({spent:.1f} s); "
+                   f"extrapolated per row class to the full pass: "
+                   f"{full_s:.0f} s"),
+        "cpu_model": cpu_model(),
+        "extrapolated_full_pass_s": full_s,
+    }
+
+
+def time_loop(fn_steps, steps, warmup, torch):
+    for _ in range(warmup):
+        fn_steps(None)
+    torch.cuda.synchronize()
+    events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        fn_steps(ev)
+        events.append(ev)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    return wall, events
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b_n128k")
+    ap.add_argument("--dense-steps", type=int, default=3)
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the "
+                          "Triangle attention pass is measured on a single "
+                          "MI355X; multi-GPU runs are not part of this build",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2507_21526_amd import binding
+    from paper_2507_21526_amd.inputs import WORKLOADS, workload_qkv
+
+    w = WORKLOADS[args.workload]
+    assert w.layers == 1, "the benchmark times one attention layer"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"drawing inputs for {w.name}")
+    q, k, v = workload_qkv(w)
+    qg, kg, vg = q.to(dev), k.to(dev), v.to(dev)
+    cu = list(w.cu_seqlens)
+
+    t0 = time.perf_counter()
+    words, info = binding.ta_build_schedule("triangle", cu, w.sink, w.window,
+                                            w.last, w.tile)
+    sched_build_us = (time.perf_counter() - t0) * 1e6
+    tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq,
+                       w.d, device=dev)
+    dense = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq,
+                         w.d, device=dev)
+    o = torch.empty(qg.shape, dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def tri_step(ev):
+        if ev is not None:
+            ev[0].record(stream)
+        binding.triangle_attn_tiles(qg, kg, vg, o, None, tri.sched, tri.info,
+                                    w.scale, tri.workspace, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        binding.triangle_attn_merge(o, None, tri.sched, tri.info,
+                                    tri.workspace, stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    def dense_step(ev):
+        if ev is not None:
+            ev[0].record(stream)
+        binding.causal_attn_fwd(qg, kg, vg, o, None, dense.sched, dense.info,
+                                w.scale, stream)
+        if ev is not None:
+            ev[1].record(stream)
+            ev[2].record(stream)
+
+    log(f"timing Triangle: {args.warmup} warmup + {args.steps} steps")
+    wall, events = time_loop(tri_step, args.steps, args.warmup, torch)
+    tile_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    merge_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
+    ms_per_step = wall * 1e3
+
+    T, d = w.tile, w.d
+    kept_flops = float(info.kept_tiles_per_qhead) * w.hq * 4.0 * T * T * d
+    value = kept_flops / (ms_per_step * 1e-3) / 1e12
+    achieved = kept_flops / (tile_ms * 1e-3) / 1e12
+
+    # merge pass: algorithmic bytes (split partials and LSE in, O out)
+    mw = words[16 + info.n_items * 12:].reshape(-1, 8)
+    part_rows = int(sum(int(r1 - r0) * int(ns) for _, r0, r1, ns, *_ in mw))
+    merge_bytes = part_rows * w.hq * (d + 1) * 4 + info.n_last_rows * w.hq * d * 2
+    merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9 if merge_ms > 0 else None
+
+    dense_rec = None
+    if not args.no_dense:
+        log(f"timing dense causal: 1 warmup + {args.dense_steps} steps")
+        dwall, devents = time_loop(dense_step, args.dense_steps, 1, torch)
+        dense_ms = dwall * 1e3
+        dense_flops = float(dense.info.kept_tiles_per_qhead) * w.hq * 4.0 * T * T * d
+        dense_rec = {
+            "ms_per_step": dense_ms,
+            "kernel_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in devents])),
+            "kept_tile_tflops": dense_flops / (dense_ms * 1e-3) / 1e12,
+            "frac_of_bf16_peak": dense_flops / (dense_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+        }
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"timing the fp64 oracle on a row sample (~{args.cpu_seconds:.0f} s)")
+        cpu = cpu_baseline(w, q, k, v, args.cpu_seconds, kept_flops)
+
+    traffic = load_traffic(w.name)
+    rec = {
+        "metric": "Triangle-attn prefill TFLOP/s (kept tiles) + speedup vs dense causal @128K",
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "cu_seqlens": cu,
+            "hq": w.hq, "hkv": w.hkv, "head_dim": d,
+            "sink": w.sink, "window": w.window, "last": w.last, "tile": T,
+            "out_dtype": "bf16",
+            "parallelism": "single-gpu",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "attn_tile_kernel (streaming + Last split items)",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic,
+            "flops_per_launch": kept_flops,
+            "kernel_ms": tile_ms,
+        },
+        "cpu_baseline": cpu,
+        "merge": {"kernel_ms": merge_ms, "algorithmic_bytes": merge_bytes,
+                  "gbs": merge_gbs, "frac_of_hbm_peak":
+                  (merge_gbs / PEAK_HBM_GBS) if merge_gbs else None},
+        "dense_causal": dense_rec,
+        "speedup_vs_dense": (dense_rec["ms_per_step"] / ms_per_step) if dense_rec else None,
+        "schedule": {"build_us_host": sched_build_us, "items": info.n_items,
+                     "kept_tiles_per_qhead": info.kept_tiles_per_qhead,
+                     "last_splits": info.max_splits},
+        "paper_context": {"speedup_128k": PAPER_SPEEDUP_128K,
+                          "hardware": "NVIDIA A100 80GB, Triton vs FlashAttention, "
+                                      "sink 8 / window 512, precision not stated"},
+        "device": torch.cuda.get_device_name(dev),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,193 @@
+/*
+ * triattn.h -- C interface of the MI355X (gfx950) Triangle attention library.
+ *
+ * Triangle attention is the static sparse prefill attention of TriangleMix
+ * (arXiv 2507.21526, Sec. 2.4): every query attends to the Streaming section
+ * (the first `sink` keys plus a causal window of `window` keys) and the last
+ * `last` queries of each sequence attend causally to every key (Last Q-K
+ * section, Appendix A.3); the Middle Q-K section is skipped.  Dense causal
+ * attention (Sec. 2.1 with the causal mask) is the path of the layers that
+ * stay dense.  The forward passes follow the split structure of Appendix A.1
+ * (Algorithm "Fused Triangle Attention"): streaming q-tiles over their sink
+ * and window k-tiles, the Last rows split over the key range, and an
+ * LSE-weighted merge of the split partials.
+ *
+ * Conventions
+ *   - Rows i and keys j are 0-indexed within a sequence of length n.  A
+ *     Triangle row keeps key j iff j <= i and (j < sink or i - j < window or
+ *     i >= n - min(last, n)).  Masked logits are excluded exactly.
+ *   - Tensors are packed "THD": q and o are [total_tokens, hq, head_dim],
+ *     k and v are [total_tokens, hkv, head_dim], contiguous, bf16 (o may be
+ *     fp32), 16-byte aligned device pointers.  Sequences are packed by
+ *     cu_seqlens[batch + 1] (cu_seqlens[0] = 0, non-decreasing).
+ *   - GQA: query head h reads kv head h / (hq / hkv).
+ *   - lse, when not NULL, is [hq, total_tokens] fp32: natural-log
+ *     log-sum-exp of the kept scaled logits of each row.
+ *   - Supported: head_dim in {64, 128}, tile in {64, 128}, hq % hkv == 0,
+ *     hq / hkv <= 8.  Others return TA_ERR_UNSUPPORTED.
+ *
+ * Ownership and synchronisation
+ *   The caller owns every buffer (inputs, outputs, the device copy of the
+ *   schedule, the workspace).  The forward functions allocate nothing, keep
+ *   no pointer after they return, never synchronise, and enqueue their
+ *   kernels on the caller's stream (a hipStream_t passed as void*; NULL is
+ *   the default stream).  Execution faults surface at the caller's next
+ *   synchronisation.
+ *
+ * Errors
+ *   Every argument is checked before any launch.  On error a function
+ *   returns a nonzero ta_status, launches nothing, leaves every output
+ *   untouched and records a message that ta_last_error() returns (per
+ *   thread).  No C++ exception crosses this interface.  The kernels also
+ *   check the schedule header against the launch arguments and write nothing
+ *   if it does not match.
+ */
+#ifndef TRIATTN_H
+#define TRIATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TA_ABI_VERSION 1
+#define TA_SCHEDULE_MAGIC 0x54524941
+#define TA_SCHEDULE_VERSION 1
+
+typedef enum {
+    TA_OK = 0,
+    TA_ERR_INVALID_ARG = 1,      /* NULL pointer, negative size, bad enum */
+    TA_ERR_UNSUPPORTED = 2,      /* valid but not implemented (head_dim...) */
+    TA_ERR_BUFFER_TOO_SMALL = 3, /* schedule output buffer too small */
+    TA_ERR_WORKSPACE = 4,        /* workspace missing or too small */
+    TA_ERR_SCHEDULE_MISMATCH = 5,/* info does not fit the call */
+    TA_ERR_HIP = 6               /* a HIP launch call failed */
+} ta_status;
+
+typedef enum { TA_KIND_TRIANGLE = 0, TA_KIND_CAUSAL = 1 } ta_kind;
+typedef enum { TA_OUT_BF16 = 0, TA_OUT_F32 = 1 } ta_out_dtype;
+
+/* Summary of a built schedule (mirrors the header words of the packed form). */
+typedef struct ta_schedule_info {
+    int32_t version;          /* TA_SCHEDULE_VERSION */
+    int32_t kind;             /* ta_kind */
+    int32_t tile;             /* T: q-tile rows = k-tile keys */
+    int32_t batch;
+    int32_t sink, window, last;
+    int32_t splits_requested; /* 0 = automatic split rule */
+    int64_t total_tokens;
+    int64_t words;            /* int32 words of the packed schedule */
+    int32_t n_items;          /* main-pass work items (Last splits first) */
+    int32_t n_last_items;     /* of which Last-row split items */
+    int32_t n_merge_items;    /* Last q-tiles (one merge each) */
+    int32_t n_last_rows;      /* rows covered by merge items */
+    int32_t n_partial_rows;   /* rows of split partials in the workspace */
+    int32_t max_splits;       /* largest split count of a Last q-tile */
+    int64_t kept_tiles_per_qhead; /* kept (q-tile, k-tile) pairs per head */
+} ta_schedule_info;
+
+/* Library interface version (TA_ABI_VERSION). */
+int32_t ta_abi_version(void);
+
+/* Message of the last non-OK status returned on this thread ("" if none). */
+const char *ta_last_error(void);
+
+/*
+ * Build the tile schedule of a pass on the host (Appendix A.1: which k-tiles
+ * each q-tile visits; Appendix A.3: the sections they cover).
+ *   kind        TA_KIND_TRIANGLE or TA_KIND_CAUSAL.
+ *   cu_seqlens  host array of batch + 1 int32 (cu_seqlens[0] = 0,
+ *               non-decreasing, cu_seqlens[batch] = total tokens).
+ *   sink >= 0, window >= 1, last >= 0 (Triangle; stored but unused for
+ *               causal).  last = 0 gives the Streaming pattern.
+ *   tile        64 or 128.
+ *   splits      0 = automatic: a Last q-tile with nk kept k-tiles gets
+ *               ceil(nk / t) splits (at most nk), t = ceil(sink/tile) +
+ *               ceil(window/tile) + 1; > 0 = that many (at most nk).
+ *   out         host buffer of out_words int32, or NULL to query the size
+ *               (info is filled either way).
+ * Returns TA_OK, TA_ERR_INVALID_ARG, TA_ERR_UNSUPPORTED or
+ * TA_ERR_BUFFER_TOO_SMALL (info->words then holds the size needed).
+ * The caller copies `out` to device memory for the forward call.
+ */
+ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
+                            int32_t batch, int32_t sink, int32_t window,
+                            int32_t last, int32_t tile, int32_t splits,
+                            int32_t *out, int64_t out_words,
+                            ta_schedule_info *info);
+
+/* Bytes of workspace triangle_attn_fwd needs for the split partials of the
+ * Last rows (fp32 partial outputs and their LSE); 0 when there are none. */
+size_t ta_workspace_bytes(const ta_schedule_info *info, int32_t hq,
+                          int32_t head_dim);
+
+/*
+ * Triangle attention forward (Sec. 2.4; Appendix A.1 and A.3).
+ *   q, k, v      bf16 device tensors in THD layout (see above).
+ *   o            [total_tokens, hq, head_dim], bf16 or fp32 per o_dtype.
+ *   lse          [hq, total_tokens] fp32 or NULL.
+ *   sched_dev    device copy of the words built by ta_build_schedule with
+ *                kind TA_KIND_TRIANGLE; info is the matching summary.
+ *   softmax_scale  multiplies q.k (1/sqrt(head_dim) in the paper).
+ *   workspace    device buffer of at least ta_workspace_bytes() bytes
+ *                (may be NULL when that is 0); its contents on entry do
+ *                not matter.
+ * Every output row (and lse entry) is written exactly once.
+ */
+ta_status triangle_attn_fwd(const void *q, const void *k, const void *v,
+                            void *o, int32_t o_dtype, float *lse,
+                            const int32_t *sched_dev,
+                            const ta_schedule_info *info, int64_t total_tokens,
+                            int32_t hq, int32_t hkv, int32_t head_dim,
+                            float softmax_scale, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+/*
+ * The two passes of triangle_attn_fwd, callable on their own (same stream
+ * order: tiles, then merge); triangle_attn_fwd is exactly these two calls.
+ *
+ * triangle_attn_tiles: the attention pass over every schedule item (Appendix
+ *   A.1: streaming q-tiles over their sink and window k-tiles; Last q-tiles
+ *   split over the key range).  Streaming rows go to o (and lse); Last rows
+ *   go to the workspace as normalised fp32 partial outputs with their LSE.
+ *   Arguments as triangle_attn_fwd.
+ * triangle_attn_merge: LSE-weighted merge of the split partials of every
+ *   Last row into o (and lse) (Appendix A.1, merge of the last-row buffers):
+ *   O = sum_c w_c O_c / sum_c w_c with w_c = exp(LSE_c - max_c LSE_c), and
+ *   LSE = max_c LSE_c + log(sum_c w_c).  Reads the workspace written by
+ *   triangle_attn_tiles with the same schedule, hq and head_dim.
+ */
+ta_status triangle_attn_tiles(const void *q, const void *k, const void *v,
+                              void *o, int32_t o_dtype, float *lse,
+                              const int32_t *sched_dev,
+                              const ta_schedule_info *info,
+                              int64_t total_tokens, int32_t hq, int32_t hkv,
+                              int32_t head_dim, float softmax_scale,
+                              void *workspace, size_t workspace_bytes,
+                              void *stream);
+ta_status triangle_attn_merge(void *o, int32_t o_dtype, float *lse,
+                              const int32_t *sched_dev,
+                              const ta_schedule_info *info,
+                              int64_t total_tokens, int32_t hq,
+                              int32_t head_dim, const void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/*
+ * Dense causal attention forward (Sec. 2.1 with the causal mask), the
+ * attention of the layers TriangleMix keeps dense.  Same arguments as
+ * triangle_attn_fwd; the schedule must be built with TA_KIND_CAUSAL.  Needs
+ * no workspace.
+ */
+ta_status causal_attn_fwd(const void *q, const void *k, const void *v,
+                          void *o, int32_t o_dtype, float *lse,
+                          const int32_t *sched_dev,
+                          const ta_schedule_info *info, int64_t total_tokens,
+                          int32_t hq, int32_t hkv, int32_t head_dim,
+                          float softmax_scale, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRIATTN_H */

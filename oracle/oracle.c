@@ -183,7 +183,8 @@ int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  * Packed int32 format (documented with the library's interface):
  *   header, 16 words: magic, version, kind, tile, batch, sink, window, last,
  *     splits requested, total_tokens (low, high 32 bits), main items, merge
- *     items, partial rows, kept k-tiles per query head, 0.
+ *     items, partial rows, kept k-tiles per query head, rows of the Last
+ *     q-tiles (the rows the merge items cover).
  *   main item, 12 words: seq_off, seq_len, r0, r1, ka0, ka1, kb0, kb1, mode,
  *     part_base, kept k-tiles, 0.   Rows [r0, r1) are relative to the
  *     sequence start; [ka0, ka1) and [kb0, kb1) are the kept k-tiles as at
@@ -282,7 +283,7 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
             return -1;
 
     item_vec last_items = {0}, main_items = {0}, merges = {0};
-    int64_t partial_rows = 0, kept_total = 0;
+    int64_t partial_rows = 0, kept_total = 0, merged_rows = 0;
     int fail = 0;
     /* steady-state streaming work of one q-tile, in k-tiles */
     const int64_t t_star = (sink + tile - 1) / tile +
@@ -356,6 +357,7 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
                              0, 0, 0}};
                 fail |= push_item(&merges, &m);
                 partial_rows += ns * (r1 - r0);
+                merged_rows += r1 - r0;
             }
             free(kept);
         }
@@ -397,7 +399,7 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
             w[12] = (int32_t)merges.n;
             w[13] = (int32_t)partial_rows;
             w[14] = (int32_t)kept_total;
-            w[15] = 0;
+            w[15] = (int32_t)merged_rows;
             w += HDR_WORDS;
             for (int64_t a = 0; a < last_items.n; ++a, w += ITEM_WORDS)
                 memcpy(w, last_items.v[a].w, sizeof(int32_t) * ITEM_WORDS);

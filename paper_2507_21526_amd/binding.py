@@ -1,0 +1,256 @@
+"""ctypes binding of libtriattn.so (include/triattn.h).
+
+Argument marshalling only: every step of the attention passes runs in the HIP
+kernels of the library.  Torch tensors provide device memory and the stream.
+The library must have been built (``python -m paper_2507_21526_amd.build``);
+loading raises ``RuntimeError`` otherwise -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtriattn.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "triattn.h")
+
+TA_OK = 0
+TA_ERR_INVALID_ARG = 1
+TA_ERR_UNSUPPORTED = 2
+TA_ERR_BUFFER_TOO_SMALL = 3
+TA_ERR_WORKSPACE = 4
+TA_ERR_SCHEDULE_MISMATCH = 5
+TA_ERR_HIP = 6
+
+TRIANGLE = 0
+CAUSAL = 1
+OUT_BF16 = 0
+OUT_F32 = 1
+
+HDR_WORDS, ITEM_WORDS, MERGE_WORDS = 16, 12, 8
+
+
+class ScheduleInfo(ctypes.Structure):
+    _fields_ = [
+        ("version", ctypes.c_int32),
+        ("kind", ctypes.c_int32),
+        ("tile", ctypes.c_int32),
+        ("batch", ctypes.c_int32),
+        ("sink", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("last", ctypes.c_int32),
+        ("splits_requested", ctypes.c_int32),
+        ("total_tokens", ctypes.c_int64),
+        ("words", ctypes.c_int64),
+        ("n_items", ctypes.c_int32),
+        ("n_last_items", ctypes.c_int32),
+        ("n_merge_items", ctypes.c_int32),
+        ("n_last_rows", ctypes.c_int32),
+        ("n_partial_rows", ctypes.c_int32),
+        ("max_splits", ctypes.c_int32),
+        ("kept_tiles_per_qhead", ctypes.c_int64),
+    ]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class TriAttnError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libtriattn.so; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with "
+            "`python -m paper_2507_21526_amd.build` (no fallback path exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    pinfo = ctypes.POINTER(ScheduleInfo)
+    L.ta_abi_version.restype = i32
+    L.ta_abi_version.argtypes = []
+    L.ta_last_error.restype = ctypes.c_char_p
+    L.ta_last_error.argtypes = []
+    L.ta_build_schedule.restype = ctypes.c_int
+    L.ta_build_schedule.argtypes = [i32, vp, i32, i32, i32, i32, i32, i32, vp,
+                                    i64, pinfo]
+    L.ta_workspace_bytes.restype = ctypes.c_size_t
+    L.ta_workspace_bytes.argtypes = [pinfo, i32, i32]
+    L.triangle_attn_fwd.restype = ctypes.c_int
+    L.triangle_attn_fwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, pinfo, i64,
+                                    i32, i32, i32, ctypes.c_float, vp,
+                                    ctypes.c_size_t, vp]
+    L.triangle_attn_tiles.restype = ctypes.c_int
+    L.triangle_attn_tiles.argtypes = list(L.triangle_attn_fwd.argtypes)
+    L.triangle_attn_merge.restype = ctypes.c_int
+    L.triangle_attn_merge.argtypes = [vp, i32, vp, vp, pinfo, i64, i32, i32,
+                                      vp, ctypes.c_size_t, vp]
+    L.causal_attn_fwd.restype = ctypes.c_int
+    L.causal_attn_fwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, pinfo, i64,
+                                  i32, i32, i32, ctypes.c_float, vp]
+    _lib = L
+    return L
+
+
+def ta_last_error() -> str:
+    return lib().ta_last_error().decode()
+
+
+def ta_abi_version() -> int:
+    return int(lib().ta_abi_version())
+
+
+def _check(status):
+    if status != TA_OK:
+        raise TriAttnError(status, ta_last_error())
+
+
+def _kind(kind) -> int:
+    if kind in (TRIANGLE, "triangle"):
+        return TRIANGLE
+    if kind in (CAUSAL, "causal"):
+        return CAUSAL
+    raise ValueError(f"unknown kind {kind!r}")
+
+
+def ta_build_schedule(kind, cu_seqlens, sink, window, last, tile, splits=0):
+    """Build a schedule on the host: returns (int32 words, ScheduleInfo)."""
+    L = lib()
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    info = ScheduleInfo()
+    _check(L.ta_build_schedule(_kind(kind), cu.ctypes.data, cu.size - 1, sink,
+                               window, last, tile, splits, None, 0,
+                               ctypes.byref(info)))
+    words = np.zeros(info.words, dtype=np.int32)
+    _check(L.ta_build_schedule(_kind(kind), cu.ctypes.data, cu.size - 1, sink,
+                               window, last, tile, splits, words.ctypes.data,
+                               words.size, ctypes.byref(info)))
+    return words, info
+
+
+def ta_workspace_bytes(info: ScheduleInfo, hq: int, head_dim: int) -> int:
+    return int(lib().ta_workspace_bytes(ctypes.byref(info), hq, head_dim))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _out_dtype(o):
+    import torch
+    if o.dtype == torch.bfloat16:
+        return OUT_BF16
+    if o.dtype == torch.float32:
+        return OUT_F32
+    raise ValueError(f"o must be bf16 or fp32, got {o.dtype}")
+
+
+def triangle_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
+                      workspace, stream=None):
+    """Enqueue Triangle attention on ``stream`` (torch current stream if None).
+
+    q [T, Hq, d], k/v [T, Hkv, d] bf16 cuda tensors; o [T, Hq, d] bf16/fp32;
+    lse [Hq, T] fp32 or None; sched_dev int32 cuda tensor of the schedule
+    words; workspace uint8 cuda tensor of >= ta_workspace_bytes bytes or None.
+    """
+    total, hq, d = q.shape
+    hkv = k.shape[1]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().triangle_attn_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
+        _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
+        float(softmax_scale), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def triangle_attn_tiles(q, k, v, o, lse, sched_dev, info, softmax_scale,
+                        workspace, stream=None):
+    """Enqueue the attention pass of Triangle attention (no merge)."""
+    total, hq, d = q.shape
+    hkv = k.shape[1]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().triangle_attn_tiles(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
+        _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
+        float(softmax_scale), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def triangle_attn_merge(o, lse, sched_dev, info, workspace, stream=None):
+    """Enqueue the merge of the Last-row split partials into o / lse."""
+    total, hq, d = o.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().triangle_attn_merge(
+        _ptr(o), _out_dtype(o), _ptr(lse), _ptr(sched_dev), ctypes.byref(info),
+        total, hq, d, _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def causal_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
+                    stream=None):
+    """Enqueue dense causal attention on ``stream``; arguments as above."""
+    total, hq, d = q.shape
+    hkv = k.shape[1]
+    _check(lib().causal_attn_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
+        _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
+        float(softmax_scale), _stream(stream)))
+
+
+class Plan:
+    """A schedule built once and uploaded to the device, plus its workspace.
+
+    Buffers come from torch; the plan can be reused for every call with the
+    same (cu_seqlens, sink, window, last, tile, splits, hq, head_dim).
+    """
+
+    def __init__(self, kind, cu_seqlens, sink, window, last, tile, hq,
+                 head_dim, splits=0, device="cuda"):
+        import torch
+        self.kind = _kind(kind)
+        self.words, self.info = ta_build_schedule(self.kind, cu_seqlens, sink,
+                                                  window, last, tile, splits)
+        self.sched = torch.from_numpy(self.words).to(device)
+        nbytes = ta_workspace_bytes(self.info, hq, head_dim)
+        self.workspace = (torch.empty(nbytes, dtype=torch.uint8, device=device)
+                          if nbytes > 0 else None)
+
+    def run(self, q, k, v, o, lse=None, softmax_scale=None, stream=None):
+        if softmax_scale is None:
+            softmax_scale = 1.0 / float(q.shape[-1]) ** 0.5
+        if self.kind == TRIANGLE:
+            triangle_attn_fwd(q, k, v, o, lse, self.sched, self.info,
+                              softmax_scale, self.workspace, stream)
+        else:
+            causal_attn_fwd(q, k, v, o, lse, self.sched, self.info,
+                            softmax_scale, stream)
+        return o
+
+
+def attention(kind, q, k, v, cu_seqlens, sink=0, window=1, last=0, tile=128,
+              splits=0, softmax_scale=None, out_dtype=None, return_lse=False):
+    """Allocate outputs with torch and run one pass (convenience wrapper)."""
+    import torch
+    out_dtype = out_dtype or torch.bfloat16
+    plan = Plan(kind, cu_seqlens, sink, window, last, tile, q.shape[1],
+                q.shape[2], splits, device=q.device)
+    o = torch.empty(q.shape, dtype=out_dtype, device=q.device)
+    lse = (torch.empty((q.shape[1], q.shape[0]), dtype=torch.float32,
+                       device=q.device) if return_lse else None)
+    plan.run(q, k, v, o, lse, softmax_scale)
+    return (o, lse) if return_lse else o

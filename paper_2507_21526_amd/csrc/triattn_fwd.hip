@@ -1,0 +1,825 @@
+// HIP forward passes of libtriattn.so for gfx950 (MI355X).
+//
+// One tile kernel serves the three attention passes of the schedule:
+//   * streaming q-tiles of Triangle attention (sink and window k-tiles,
+//     Appendix A.1 upper part; streaming mask of Appendix A.3),
+//   * Last-row split items (one contiguous chunk of k-tiles of a Last q-tile,
+//     Appendix A.1 lower part), writing normalised fp32 partials and LSE,
+//   * q-tiles of dense causal attention (Sec. 2.1, causal mask).
+// A second kernel merges the split partials of the Last rows with LSE
+// weights (Appendix A.1, merge of the last-row buffers).
+//
+// Tile core (flash-style online softmax, Sec. 2.1 evaluated blockwise):
+//   A workgroup owns one work item, one kv head g and R query rows of each of
+//   the G query heads of g, so every K/V tile staged in LDS is shared by the
+//   whole GQA group.  Each wave owns 32 query rows of one head.  Keys advance
+//   in steps of 64.  The wave computes S^T = K Q^T with bf16 MFMA 32x32x16
+//   (keys on the MFMA rows, queries on the columns), so a lane holds 32
+//   scores of a single query: the softmax max/sum are in-lane plus one swap
+//   between the two lane halves.  The K rows fed to the MFMA are permuted
+//   (bits 2 and 3 of the row index swapped) so that the score registers are
+//   directly the B operand of O^T += V^T P^T, with V staged transposed in
+//   LDS.  Softmax runs in the log2 domain with fp32 state.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "triattn_internal.h"
+
+namespace triattn {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kStep = 64;  // keys per inner step
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+struct FwdArgs {
+    const uint16_t *q;
+    const uint16_t *k;
+    const uint16_t *v;
+    void *o;
+    float *lse;
+    const int32_t *sched;
+    float *part_o;    // [partial rows, hq, d] fp32
+    float *part_lse;  // [partial rows, hq] fp32
+    int64_t total_tokens;
+    int32_t hq, hkv, group;
+    int32_t n_items;
+    int32_t n_partial_rows;
+    int32_t sink, window;
+    int32_t tile;
+    int32_t rows_per_wg;  // R
+    int32_t subtiles;     // tile / R
+    int32_t o_f32;
+    float scale_log2;     // softmax scale * log2(e)
+};
+
+struct MergeArgs {
+    const int32_t *sched;
+    const float *part_o;
+    const float *part_lse;
+    void *o;
+    float *lse;
+    int64_t total_tokens;
+    int32_t hq;
+    int32_t n_items;
+    int32_t n_merges;
+    int32_t n_partial_rows;
+    int32_t n_last_rows;
+    int32_t o_f32;
+};
+
+__device__ __forceinline__ bool header_ok(const int32_t *s, int64_t total,
+                                          int32_t n_items, int32_t kind)
+{
+    const int64_t t = (int64_t)(uint32_t)s[H_TOTAL_LO] |
+                      ((int64_t)s[H_TOTAL_HI] << 32);
+    return s[H_MAGIC] == TA_SCHEDULE_MAGIC &&
+           s[H_VERSION] == TA_SCHEDULE_VERSION && s[H_KIND] == kind &&
+           t == total && s[H_ITEMS] == n_items;
+}
+
+// Key offset (within a 32-key block) held by register v of lane half h in
+// the S^T accumulator, given the permuted K row order.
+__device__ __forceinline__ int key_of_reg(int v, int h)
+{
+    return (v & 7) + 8 * h + 16 * (v >> 3);
+}
+
+// Permuted K row for MFMA row r: swap bits 2 and 3.
+__device__ __forceinline__ int perm_row(int r)
+{
+    return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+__device__ __forceinline__ float pair_max(float x)
+{
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                              __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float pair_sum(float x)
+{
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x),
+                                              __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t kind)
+{
+    constexpr int NT = NW * 64;
+    constexpr int KS = D + 8;      // K row stride in LDS (bf16 elements)
+    constexpr int VS = kStep + 8;  // V^T row stride in LDS (bf16 elements)
+    constexpr int K_ELEMS = kStep * KS;
+    constexpr int V_ELEMS = D * VS;
+    constexpr int STAGE = K_ELEMS + V_ELEMS;
+    constexpr int DCH = D / 8;                     // 16-byte chunks per row
+    constexpr int K_CHUNKS = kStep * DCH;          // K tile chunks
+    constexpr int V_CHUNKS = (kStep / 2) * DCH;    // V tile key-pair chunks
+    constexpr int K_LOADS = (K_CHUNKS + NT - 1) / NT;
+    constexpr int V_LOADS = (V_CHUNKS + NT - 1) / NT;
+    constexpr int QK_STEPS = D / 16;
+    constexpr int D_BLOCKS = D / 32;
+
+    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * STAGE];
+
+    const int32_t *sched = a.sched;
+    if (!header_ok(sched, a.total_tokens, a.n_items, kind))
+        return;
+
+    int bid = blockIdx.x;
+    const int g = bid % a.hkv;
+    bid /= a.hkv;
+    const int sub = bid % a.subtiles;
+    const int item = bid / a.subtiles;
+    if (item >= a.n_items)
+        return;
+    const int32_t *it = sched + kHdrWords + (int64_t)item * kItemWords;
+    const int64_t seq_off = it[I_SEQ_OFF];
+    const int32_t seq_len = it[I_SEQ_LEN];
+    const int32_t r0 = it[I_R0], r1 = it[I_R1];
+    const int32_t ka0 = it[I_KA0], ka1 = it[I_KA1];
+    const int32_t kb0 = it[I_KB0], kb1 = it[I_KB1];
+    const int32_t mode = it[I_MODE];
+    const int32_t part_base = it[I_PART_BASE];
+    // Guard against a malformed schedule: never touch memory outside it.
+    if (seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
+        r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || ka1 < ka0 ||
+        kb0 < 0 || kb1 < kb0 ||
+        (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows))
+        return;
+
+    const int wr0 = r0 + sub * a.rows_per_wg;  // first row of this workgroup
+    if (wr0 >= r1)
+        return;  // ragged q-tile: nothing for this workgroup
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int half = lane >> 5;
+    const int col = lane & 31;
+    const int waves_per_head = a.rows_per_wg / 32;
+    const int head = g * a.group + wave / waves_per_head;
+    const int row_base = wr0 + (wave % waves_per_head) * 32;
+    const bool wave_active = row_base < r1;
+    const int my_row = row_base + col;            // sequence-relative row
+    const bool row_valid = my_row < r1;
+    const int load_row = row_valid ? my_row : r1 - 1;
+    const int row_hi = (r1 - 1 < row_base + 31) ? r1 - 1 : row_base + 31;
+
+    // Steps of 64 keys over the kept k-tiles.
+    const int tps = a.tile / kStep;
+    const int na = (ka1 - ka0) * tps;
+    const int nsteps = na + (kb1 - kb0) * tps;
+    auto step_key0 = [&](int s) -> int {
+        return s < na ? (ka0 * tps + s) * kStep : (kb0 * tps + (s - na)) * kStep;
+    };
+
+    // Q fragments (B operand of S^T = K Q^T): lane holds Q[row][16s + 8h ..].
+    bf16x8 qf[QK_STEPS];
+    {
+        const uint16_t *qp = a.q + ((seq_off + load_row) * a.hq + head) * (int64_t)D +
+                             8 * half;
+#pragma unroll
+        for (int s = 0; s < QK_STEPS; ++s)
+            qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
+    }
+
+    const uint16_t *kbase = a.k + (seq_off * a.hkv + g) * (int64_t)D;
+    const uint16_t *vbase = a.v + (seq_off * a.hkv + g) * (int64_t)D;
+    const int64_t tok_stride = (int64_t)a.hkv * D;
+
+    u32x4 kreg[K_LOADS];
+    u32x4 vreg[V_LOADS][2];
+
+    auto load_tile = [&](int key0) {
+#pragma unroll
+        for (int i = 0; i < K_LOADS; ++i) {
+            const int c = tid + i * NT;
+            if (c < K_CHUNKS) {
+                const int key = key0 + c / DCH;
+                const int dc = c % DCH;
+                if (key < seq_len)
+                    kreg[i] = *reinterpret_cast<const u32x4 *>(
+                        kbase + key * tok_stride + dc * 8);
+                else
+                    kreg[i] = u32x4{0, 0, 0, 0};
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < V_LOADS; ++i) {
+            const int c = tid + i * NT;
+            if (c < V_CHUNKS) {
+                const int kp = c % (kStep / 2);
+                const int dc = c / (kStep / 2);
+                const int key = key0 + 2 * kp;
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    if (key + e < seq_len)
+                        vreg[i][e] = *reinterpret_cast<const u32x4 *>(
+                            vbase + (key + e) * tok_stride + dc * 8);
+                    else
+                        vreg[i][e] = u32x4{0, 0, 0, 0};
+                }
+            }
+        }
+    };
+
+    auto store_tile = [&](int buf) {
+        uint16_t *kl = smem + buf * STAGE;
+        uint32_t *vl = reinterpret_cast<uint32_t *>(kl + K_ELEMS);
+#pragma unroll
+        for (int i = 0; i < K_LOADS; ++i) {
+            const int c = tid + i * NT;
+            if (c < K_CHUNKS) {
+                const int key = c / DCH, dc = c % DCH;
+                *reinterpret_cast<u32x4 *>(kl + key * KS + dc * 8) = kreg[i];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < V_LOADS; ++i) {
+            const int c = tid + i * NT;
+            if (c < V_CHUNKS) {
+                const int kp = c % (kStep / 2);
+                const int dc = c / (kStep / 2);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    // element e of each key's chunk: pack (key 2kp, key 2kp+1)
+                    const uint32_t lo = (vreg[i][0][e >> 1] >> (16 * (e & 1))) & 0xffffu;
+                    const uint32_t hi = (vreg[i][1][e >> 1] >> (16 * (e & 1))) & 0xffffu;
+                    vl[((dc * 8 + e) * VS) / 2 + kp] = lo | (hi << 16);
+                }
+            }
+        }
+    };
+
+    f32x16 oacc[D_BLOCKS];
+#pragma unroll
+    for (int b = 0; b < D_BLOCKS; ++b)
+        oacc[b] = f32x16{};
+    float m_run = -INFINITY;  // running max, log2 domain (scaled)
+    float l_run = 0.f;        // running sum, this lane's keys only
+
+    if (nsteps > 0) {
+        load_tile(step_key0(0));
+        store_tile(0);
+    }
+    __syncthreads();
+
+    for (int st = 0; st < nsteps; ++st) {
+        const int buf = st & 1;
+        const int key0 = step_key0(st);
+        const bool more = st + 1 < nsteps;
+        if (more)
+            load_tile(step_key0(st + 1));
+
+        // Is any (row, key) pair of this wave kept in this step?
+        bool any = wave_active && key0 <= row_hi;
+        if (any && mode == kModeStreaming)
+            any = (key0 < a.sink) || (row_base - (key0 + kStep - 1) < a.window);
+        if (any) {
+            const uint16_t *kl = smem + buf * STAGE;
+            const uint16_t *vl = kl + K_ELEMS;
+            f32x16 sacc[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                sacc[kb] = f32x16{};
+                const uint16_t *kr = kl + (kb * 32 + perm_row(col)) * KS + 8 * half;
+#pragma unroll
+                for (int s = 0; s < QK_STEPS; ++s) {
+                    const bf16x8 af = *reinterpret_cast<const bf16x8 *>(kr + 16 * s);
+                    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[s],
+                                                                      sacc[kb], 0, 0, 0);
+                }
+            }
+
+            // Element mask where the step crosses the diagonal or the window.
+            const bool need_mask =
+                (key0 + kStep - 1 > row_base) ||
+                (mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
+                 row_hi - key0 >= a.window);
+            if (need_mask) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int key = key0 + kb * 32 + key_of_reg(v, half);
+                        bool keep = key <= my_row;
+                        if (mode == kModeStreaming)
+                            keep = keep && (key < a.sink || my_row - key < a.window);
+                        if (!keep)
+                            sacc[kb][v] = -INFINITY;
+                    }
+            }
+
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    mx = fmaxf(mx, sacc[kb][v]);
+            mx = pair_max(mx);
+            const float m_new = fmaxf(m_run, mx * a.scale_log2);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+            m_run = m_new;
+
+            float psum = 0.f;
+            bf16x8 pf[2][2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const float p = __builtin_amdgcn_exp2f(
+                        __builtin_fmaf(sacc[kb][v], a.scale_log2, -m_use));
+                    sacc[kb][v] = p;
+                    psum += p;
+                }
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    f32x8 t;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        t[e] = sacc[kb][8 * s2 + e];
+                    pf[kb][s2] = __builtin_convertvector(t, bf16x8);
+                }
+            }
+            l_run = l_run * alpha + psum;
+#pragma unroll
+            for (int b = 0; b < D_BLOCKS; ++b)
+                oacc[b] *= alpha;
+
+#pragma unroll
+            for (int b = 0; b < D_BLOCKS; ++b) {
+                const uint16_t *vr = vl + (b * 32 + col) * VS + 8 * half;
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int s2 = 0; s2 < 2; ++s2) {
+                        const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
+                            vr + kb * 32 + s2 * 16);
+                        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            af, pf[kb][s2], oacc[b], 0, 0, 0);
+                    }
+            }
+        }
+
+        if (more)
+            store_tile(buf ^ 1);
+        __syncthreads();
+    }
+
+    if (!wave_active)
+        return;
+    const float l_tot = pair_sum(l_run);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float row_lse = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (!row_valid)
+        return;
+
+    if (part_base >= 0) {
+        const int64_t prow = (int64_t)(part_base + (my_row - r0)) * a.hq + head;
+        float *po = a.part_o + prow * D;
+#pragma unroll
+        for (int b = 0; b < D_BLOCKS; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                f32x4 t;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    t[e] = oacc[b][4 * j + e] * inv;
+                *reinterpret_cast<f32x4 *>(po + b * 32 + 8 * j + 4 * half) = t;
+            }
+        if (half == 0)
+            a.part_lse[prow] = row_lse;
+        return;
+    }
+
+    const int64_t orow = ((seq_off + my_row) * a.hq + head) * (int64_t)D;
+    if (a.o_f32) {
+        float *op = reinterpret_cast<float *>(a.o) + orow;
+#pragma unroll
+        for (int b = 0; b < D_BLOCKS; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                f32x4 t;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    t[e] = oacc[b][4 * j + e] * inv;
+                *reinterpret_cast<f32x4 *>(op + b * 32 + 8 * j + 4 * half) = t;
+            }
+    } else {
+        __bf16 *op = reinterpret_cast<__bf16 *>(a.o) + orow;
+#pragma unroll
+        for (int b = 0; b < D_BLOCKS; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                f32x4 t;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    t[e] = oacc[b][4 * j + e] * inv;
+                *reinterpret_cast<bf16x4 *>(op + b * 32 + 8 * j + 4 * half) =
+                    __builtin_convertvector(t, bf16x4);
+            }
+    }
+    if (a.lse && half == 0)
+        a.lse[(int64_t)head * a.total_tokens + seq_off + my_row] = row_lse;
+}
+
+// LSE-weighted merge of the split partials of the Last rows.  One wave per
+// (Last row, query head): the wave reduces max and sum of the split LSEs
+// across its lanes, then accumulates the weighted partial rows.
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
+{
+    const int32_t *sched = a.sched;
+    if (!header_ok(sched, a.total_tokens, a.n_items, TA_KIND_TRIANGLE))
+        return;
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= (int64_t)a.n_last_rows * a.hq)
+        return;
+    const int head = (int)(w % a.hq);
+    int64_t rank = w / a.hq;  // index among all Last rows
+
+    const int32_t *mi = sched + kHdrWords + (int64_t)a.n_items * kItemWords;
+    int m = 0;
+    for (; m < a.n_merges; ++m) {
+        const int32_t *x = mi + (int64_t)m * kMergeWords;
+        const int rows = x[M_R1] - x[M_R0];
+        if (rank < rows)
+            break;
+        rank -= rows;
+    }
+    if (m >= a.n_merges)
+        return;
+    const int32_t *x = mi + (int64_t)m * kMergeWords;
+    const int64_t seq_off = x[M_SEQ_OFF];
+    const int32_t r0 = x[M_R0], r1 = x[M_R1], ns = x[M_SPLITS], pb = x[M_PART_BASE];
+    const int rows = r1 - r0;
+    if (ns < 1 || pb < 0 || pb + (int64_t)ns * rows > a.n_partial_rows ||
+        seq_off + r1 > a.total_tokens)
+        return;
+    const int row = r0 + (int)rank;
+
+    auto lse_of = [&](int c) -> float {
+        return a.part_lse[((int64_t)pb + (int64_t)c * rows + rank) * a.hq + head];
+    };
+    float mx = -INFINITY;
+    for (int c = lane; c < ns; c += 64)
+        mx = fmaxf(mx, lse_of(c));
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        mx = fmaxf(mx, __shfl_xor(mx, off));
+    const float m_use = (mx == -INFINITY) ? 0.f : mx;
+    float den = 0.f;
+    for (int c = lane; c < ns; c += 64)
+        den += __expf(lse_of(c) - m_use);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        den += __shfl_xor(den, off);
+
+    constexpr int PER = D / 64;  // elements per lane
+    float acc[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e)
+        acc[e] = 0.f;
+    for (int c = 0; c < ns; ++c) {
+        const float wgt = __expf(lse_of(c) - m_use);
+        const float *po =
+            a.part_o + (((int64_t)pb + (int64_t)c * rows + rank) * a.hq + head) * D;
+        if constexpr (PER == 2) {
+            const f32x2 t = *reinterpret_cast<const f32x2 *>(po + 2 * lane);
+            acc[0] += wgt * t[0];
+            acc[PER - 1] += wgt * t[1];
+        } else {
+            acc[0] += wgt * po[lane];
+        }
+    }
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    const int64_t orow = ((seq_off + row) * a.hq + head) * (int64_t)D;
+    if (a.o_f32) {
+        float *op = reinterpret_cast<float *>(a.o) + orow;
+        if constexpr (PER == 2) {
+            f32x2 t = {acc[0] * inv, acc[PER - 1] * inv};
+            *reinterpret_cast<f32x2 *>(op + 2 * lane) = t;
+        } else {
+            op[lane] = acc[0] * inv;
+        }
+    } else {
+        __bf16 *op = reinterpret_cast<__bf16 *>(a.o) + orow;
+        if constexpr (PER == 2) {
+            f32x2 t = {acc[0] * inv, acc[PER - 1] * inv};
+            *reinterpret_cast<bf16x2 *>(op + 2 * lane) = __builtin_convertvector(t, bf16x2);
+        } else {
+            op[lane] = (__bf16)(acc[0] * inv);
+        }
+    }
+    if (a.lse && lane == 0)
+        a.lse[(int64_t)head * a.total_tokens + seq_off + row] =
+            den > 0.f ? m_use + __logf(den) : -INFINITY;
+}
+
+// Rows per workgroup: the largest of 128, 64, 32 that divides the tile and
+// keeps G * R / 32 <= 8 waves.
+int rows_per_wg(int group, int tile)
+{
+    for (int r = 128; r >= 32; r /= 2)
+        if (r <= tile && group * r / 32 <= 8)
+            return r;
+    return 32;
+}
+
+template <int D>
+hipError_t launch_tile(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_t s)
+{
+    switch (nw) {
+    case 1: hipLaunchKernelGGL((attn_tile_kernel<D, 1>), grid, dim3(64), 0, s, a, kind); break;
+    case 2: hipLaunchKernelGGL((attn_tile_kernel<D, 2>), grid, dim3(128), 0, s, a, kind); break;
+    case 3: hipLaunchKernelGGL((attn_tile_kernel<D, 3>), grid, dim3(192), 0, s, a, kind); break;
+    case 4: hipLaunchKernelGGL((attn_tile_kernel<D, 4>), grid, dim3(256), 0, s, a, kind); break;
+    case 5: hipLaunchKernelGGL((attn_tile_kernel<D, 5>), grid, dim3(320), 0, s, a, kind); break;
+    case 6: hipLaunchKernelGGL((attn_tile_kernel<D, 6>), grid, dim3(384), 0, s, a, kind); break;
+    case 7: hipLaunchKernelGGL((attn_tile_kernel<D, 7>), grid, dim3(448), 0, s, a, kind); break;
+    case 8: hipLaunchKernelGGL((attn_tile_kernel<D, 8>), grid, dim3(512), 0, s, a, kind); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+ta_status check_common(const char *fn, int want_kind, const void *q, const void *k,
+                       const void *v, void *o, int32_t o_dtype,
+                       const int32_t *sched_dev, const ta_schedule_info *info,
+                       int64_t total_tokens, int32_t hq, int32_t hkv,
+                       int32_t head_dim, float scale)
+{
+    if (!info)
+        return fail(TA_ERR_INVALID_ARG, "%s: info is NULL", fn);
+    if (info->version != TA_SCHEDULE_VERSION)
+        return fail(TA_ERR_SCHEDULE_MISMATCH, "%s: schedule version %d != %d", fn,
+                    info->version, TA_SCHEDULE_VERSION);
+    if (info->kind != want_kind)
+        return fail(TA_ERR_SCHEDULE_MISMATCH, "%s: schedule kind %d, need %d", fn,
+                    info->kind, want_kind);
+    if (total_tokens < 0)
+        return fail(TA_ERR_INVALID_ARG, "%s: total_tokens < 0", fn);
+    if (info->total_tokens != total_tokens)
+        return fail(TA_ERR_SCHEDULE_MISMATCH,
+                    "%s: schedule built for %lld tokens, call has %lld", fn,
+                    (long long)info->total_tokens, (long long)total_tokens);
+    if (hq <= 0 || hkv <= 0)
+        return fail(TA_ERR_INVALID_ARG, "%s: hq and hkv must be positive", fn);
+    if (hq % hkv != 0)
+        return fail(TA_ERR_INVALID_ARG, "%s: hq %d not a multiple of hkv %d", fn, hq, hkv);
+    if (hq / hkv > 8)
+        return fail(TA_ERR_UNSUPPORTED, "%s: GQA group %d > 8", fn, hq / hkv);
+    if (head_dim != 64 && head_dim != 128)
+        return fail(TA_ERR_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
+    if (info->tile != 64 && info->tile != 128)
+        return fail(TA_ERR_UNSUPPORTED, "%s: tile %d not in {64, 128}", fn, info->tile);
+    if (o_dtype != TA_OUT_BF16 && o_dtype != TA_OUT_F32)
+        return fail(TA_ERR_INVALID_ARG, "%s: bad o_dtype %d", fn, o_dtype);
+    if (!std::isfinite(scale) || !(scale > 0.f))
+        return fail(TA_ERR_INVALID_ARG, "%s: softmax_scale must be finite and > 0", fn);
+    if (info->n_items < 0 || info->n_merge_items < 0 || info->n_partial_rows < 0 ||
+        info->n_last_rows < 0)
+        return fail(TA_ERR_SCHEDULE_MISMATCH, "%s: corrupt schedule info", fn);
+    if (total_tokens > 0 || info->n_items > 0) {
+        if (!q || !k || !v || !o || !sched_dev)
+            return fail(TA_ERR_INVALID_ARG, "%s: NULL q, k, v, o or schedule", fn);
+        if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o) & 15)
+            return fail(TA_ERR_INVALID_ARG, "%s: q, k, v and o must be 16-byte aligned", fn);
+    }
+    const int64_t subtiles = info->tile / rows_per_wg(hq / hkv, info->tile);
+    if ((int64_t)info->n_items * subtiles * hkv > INT32_MAX)
+        return fail(TA_ERR_UNSUPPORTED, "%s: grid too large", fn);
+    return TA_OK;
+}
+
+FwdArgs make_args(const void *q, const void *k, const void *v, void *o,
+                  int32_t o_dtype, float *lse, const int32_t *sched_dev,
+                  const ta_schedule_info *info, int64_t total_tokens, int32_t hq,
+                  int32_t hkv, float scale, float *part_o, float *part_lse)
+{
+    const int group = hq / hkv;
+    const int R = rows_per_wg(group, info->tile);
+    FwdArgs a;
+    a.q = static_cast<const uint16_t *>(q);
+    a.k = static_cast<const uint16_t *>(k);
+    a.v = static_cast<const uint16_t *>(v);
+    a.o = o;
+    a.lse = lse;
+    a.sched = sched_dev;
+    a.part_o = part_o;
+    a.part_lse = part_lse;
+    a.total_tokens = total_tokens;
+    a.hq = hq;
+    a.hkv = hkv;
+    a.group = group;
+    a.n_items = info->n_items;
+    a.n_partial_rows = info->n_partial_rows;
+    a.sink = info->sink;
+    a.window = info->window;
+    a.tile = info->tile;
+    a.rows_per_wg = R;
+    a.subtiles = info->tile / R;
+    a.o_f32 = o_dtype == TA_OUT_F32;
+    a.scale_log2 = scale * kLog2e;
+    return a;
+}
+
+ta_status launch_tiles(int kind, const FwdArgs &a, int32_t head_dim, hipStream_t stream)
+{
+    if (a.n_items <= 0)
+        return TA_OK;
+    const int nw = a.group * a.rows_per_wg / 32;
+    dim3 grid((unsigned)((int64_t)a.n_items * a.subtiles * a.hkv));
+    hipError_t err = head_dim == 128 ? launch_tile<128>(nw, grid, a, kind, stream)
+                                     : launch_tile<64>(nw, grid, a, kind, stream);
+    if (err != hipSuccess)
+        return fail(TA_ERR_HIP, "attention tile kernel launch failed: %s",
+                    hipGetErrorString(err));
+    return TA_OK;
+}
+
+ta_status launch_merge(void *o, int32_t o_dtype, float *lse, const int32_t *sched_dev,
+                       const ta_schedule_info *info, int64_t total_tokens, int32_t hq,
+                       int32_t head_dim, const float *part_o, const float *part_lse,
+                       hipStream_t stream)
+{
+    if (info->n_merge_items <= 0 || info->n_last_rows <= 0)
+        return TA_OK;
+    MergeArgs m;
+    m.sched = sched_dev;
+    m.part_o = part_o;
+    m.part_lse = part_lse;
+    m.o = o;
+    m.lse = lse;
+    m.total_tokens = total_tokens;
+    m.hq = hq;
+    m.n_items = info->n_items;
+    m.n_merges = info->n_merge_items;
+    m.n_partial_rows = info->n_partial_rows;
+    m.n_last_rows = info->n_last_rows;
+    m.o_f32 = o_dtype == TA_OUT_F32;
+    const int64_t waves = (int64_t)info->n_last_rows * hq;
+    dim3 grid((unsigned)((waves + 3) / 4));
+    if (head_dim == 128)
+        hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, m);
+    else
+        hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, m);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess)
+        return fail(TA_ERR_HIP, "merge kernel launch failed: %s", hipGetErrorString(err));
+    return TA_OK;
+}
+
+// Split the caller's workspace into the partial outputs and their LSE.
+ta_status resolve_workspace(const char *fn, const ta_schedule_info *info, int32_t hq,
+                            int32_t head_dim, const void *workspace,
+                            size_t workspace_bytes, float **part_o, float **part_lse)
+{
+    *part_o = nullptr;
+    *part_lse = nullptr;
+    const size_t need = ta_workspace_bytes(info, hq, head_dim);
+    if (need == 0)
+        return TA_OK;
+    if (!workspace || workspace_bytes < need)
+        return fail(TA_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, got %zu%s", fn,
+                    need, workspace_bytes, workspace ? "" : " (NULL)");
+    if ((uintptr_t)workspace & 15)
+        return fail(TA_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", fn);
+    const size_t rows = (size_t)info->n_partial_rows * (size_t)hq;
+    const size_t o_bytes = (rows * (size_t)head_dim * 4 + 255) & ~(size_t)255;
+    *part_o = static_cast<float *>(const_cast<void *>(workspace));
+    *part_lse = reinterpret_cast<float *>(static_cast<char *>(const_cast<void *>(workspace)) +
+                                          o_bytes);
+    return TA_OK;
+}
+
+}  // namespace
+}  // namespace triattn
+
+using namespace triattn;
+
+extern "C" ta_status triangle_attn_tiles(const void *q, const void *k, const void *v,
+                                         void *o, int32_t o_dtype, float *lse,
+                                         const int32_t *sched_dev,
+                                         const ta_schedule_info *info,
+                                         int64_t total_tokens, int32_t hq, int32_t hkv,
+                                         int32_t head_dim, float softmax_scale,
+                                         void *workspace, size_t workspace_bytes,
+                                         void *stream)
+{
+    clear_error();
+    ta_status st = check_common("triangle_attn_tiles", TA_KIND_TRIANGLE, q, k, v, o,
+                                o_dtype, sched_dev, info, total_tokens, hq, hkv,
+                                head_dim, softmax_scale);
+    if (st != TA_OK)
+        return st;
+    float *part_o, *part_lse;
+    st = resolve_workspace("triangle_attn_tiles", info, hq, head_dim, workspace,
+                           workspace_bytes, &part_o, &part_lse);
+    if (st != TA_OK)
+        return st;
+    const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
+                                hq, hkv, softmax_scale, part_o, part_lse);
+    return launch_tiles(TA_KIND_TRIANGLE, a, head_dim, static_cast<hipStream_t>(stream));
+}
+
+extern "C" ta_status triangle_attn_merge(void *o, int32_t o_dtype, float *lse,
+                                         const int32_t *sched_dev,
+                                         const ta_schedule_info *info,
+                                         int64_t total_tokens, int32_t hq,
+                                         int32_t head_dim, const void *workspace,
+                                         size_t workspace_bytes, void *stream)
+{
+    clear_error();
+    static const char fn[] = "triangle_attn_merge";
+    if (!info)
+        return fail(TA_ERR_INVALID_ARG, "%s: info is NULL", fn);
+    if (info->version != TA_SCHEDULE_VERSION || info->kind != TA_KIND_TRIANGLE)
+        return fail(TA_ERR_SCHEDULE_MISMATCH, "%s: need a Triangle schedule (version %d)",
+                    fn, TA_SCHEDULE_VERSION);
+    if (info->total_tokens != total_tokens)
+        return fail(TA_ERR_SCHEDULE_MISMATCH,
+                    "%s: schedule built for %lld tokens, call has %lld", fn,
+                    (long long)info->total_tokens, (long long)total_tokens);
+    if (hq <= 0)
+        return fail(TA_ERR_INVALID_ARG, "%s: hq must be positive", fn);
+    if (head_dim != 64 && head_dim != 128)
+        return fail(TA_ERR_UNSUPPORTED, "%s: head_dim %d not in {64, 128}", fn, head_dim);
+    if (o_dtype != TA_OUT_BF16 && o_dtype != TA_OUT_F32)
+        return fail(TA_ERR_INVALID_ARG, "%s: bad o_dtype %d", fn, o_dtype);
+    if (info->n_merge_items > 0 && (!o || !sched_dev))
+        return fail(TA_ERR_INVALID_ARG, "%s: NULL o or schedule", fn);
+    if ((uintptr_t)o & 15)
+        return fail(TA_ERR_INVALID_ARG, "%s: o must be 16-byte aligned", fn);
+    float *part_o, *part_lse;
+    ta_status st = resolve_workspace(fn, info, hq, head_dim, workspace, workspace_bytes,
+                                     &part_o, &part_lse);
+    if (st != TA_OK)
+        return st;
+    return launch_merge(o, o_dtype, lse, sched_dev, info, total_tokens, hq, head_dim,
+                        part_o, part_lse, static_cast<hipStream_t>(stream));
+}
+
+extern "C" ta_status triangle_attn_fwd(const void *q, const void *k, const void *v,
+                                       void *o, int32_t o_dtype, float *lse,
+                                       const int32_t *sched_dev,
+                                       const ta_schedule_info *info,
+                                       int64_t total_tokens, int32_t hq, int32_t hkv,
+                                       int32_t head_dim, float softmax_scale,
+                                       void *workspace, size_t workspace_bytes,
+                                       void *stream)
+{
+    clear_error();
+    ta_status st = check_common("triangle_attn_fwd", TA_KIND_TRIANGLE, q, k, v, o,
+                                o_dtype, sched_dev, info, total_tokens, hq, hkv,
+                                head_dim, softmax_scale);
+    if (st != TA_OK)
+        return st;
+    float *part_o, *part_lse;
+    st = resolve_workspace("triangle_attn_fwd", info, hq, head_dim, workspace,
+                           workspace_bytes, &part_o, &part_lse);
+    if (st != TA_OK)
+        return st;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
+                                hq, hkv, softmax_scale, part_o, part_lse);
+    st = launch_tiles(TA_KIND_TRIANGLE, a, head_dim, s);
+    if (st != TA_OK)
+        return st;
+    return launch_merge(o, o_dtype, lse, sched_dev, info, total_tokens, hq, head_dim,
+                        part_o, part_lse, s);
+}
+
+extern "C" ta_status causal_attn_fwd(const void *q, const void *k, const void *v,
+                                     void *o, int32_t o_dtype, float *lse,
+                                     const int32_t *sched_dev,
+                                     const ta_schedule_info *info, int64_t total_tokens,
+                                     int32_t hq, int32_t hkv, int32_t head_dim,
+                                     float softmax_scale, void *stream)
+{
+    clear_error();
+    ta_status st = check_common("causal_attn_fwd", TA_KIND_CAUSAL, q, k, v, o, o_dtype,
+                                sched_dev, info, total_tokens, hq, hkv, head_dim,
+                                softmax_scale);
+    if (st != TA_OK)
+        return st;
+    const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
+                                hq, hkv, softmax_scale, nullptr, nullptr);
+    return launch_tiles(TA_KIND_CAUSAL, a, head_dim, static_cast<hipStream_t>(stream));
+}

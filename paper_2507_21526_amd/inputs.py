@@ -2,9 +2,9 @@
 
 This module holds no attention arithmetic: it draws the Q/K/V tensors that
 both the HIP path and the CPU oracle consume, so that the two sides read the
-same bf16 bytes.  Values are drawn in fp32 from a seeded CPU
-``torch.Generator`` (i.i.d. N(0, 1), optionally scaled per head or with a
-boosted key 0) and rounded once to bf16 (round to nearest even).
+same bf16 bytes.  Values are drawn in fp32 from a seeded numpy PCG64
+generator (i.i.d. N(0, 1), optionally scaled per head or with a boosted
+key 0) and rounded once to bf16 (round to nearest even).
 
 The workloads stand in for the attention-kernel latency measurements of the
 paper (Sec. 3.4, table of attention kernel latency: Llama-3.1-8B and
@@ -16,6 +16,7 @@ from __future__ import annotations
 import math
 from dataclasses import dataclass, field
 
+import numpy as np
 import torch
 
 
@@ -75,27 +76,27 @@ def draw_qkv(cu_seqlens, hq: int, hkv: int, d: int, seed: int,
              head_scale=None, key0_boost=None):
     """Seeded bf16 Q [T, Hq, d], K and V [T, Hkv, d] on the CPU.
 
-    Draw order from one generator: Q, K, V (N(0, 1) fp32), then, if
-    ``head_scale`` is given, per-head factors U[lo, hi] for Q (Hq values),
+    Draw order from one numpy PCG64 generator: Q, K, V (N(0, 1) fp32), then,
+    if ``head_scale`` is given, per-head factors U[lo, hi] for Q (Hq values),
     K and V (Hkv values each).  ``key0_boost`` multiplies the key of token 0
     of every kv head.  A single rounding to bf16 ends the draw.
     """
     total = int(cu_seqlens[-1])
-    gen = torch.Generator(device="cpu").manual_seed(int(seed))
-    q = torch.randn((total, hq, d), generator=gen, dtype=torch.float32)
-    k = torch.randn((total, hkv, d), generator=gen, dtype=torch.float32)
-    v = torch.randn((total, hkv, d), generator=gen, dtype=torch.float32)
+    rng = np.random.default_rng(int(seed))
+    q = rng.standard_normal((total, hq, d), dtype=np.float32)
+    k = rng.standard_normal((total, hkv, d), dtype=np.float32)
+    v = rng.standard_normal((total, hkv, d), dtype=np.float32)
     if head_scale is not None:
         lo, hi = head_scale
-        sq = lo + (hi - lo) * torch.rand(hq, generator=gen, dtype=torch.float32)
-        sk = lo + (hi - lo) * torch.rand(hkv, generator=gen, dtype=torch.float32)
-        sv = lo + (hi - lo) * torch.rand(hkv, generator=gen, dtype=torch.float32)
-        q.mul_(sq.view(1, hq, 1))
-        k.mul_(sk.view(1, hkv, 1))
-        v.mul_(sv.view(1, hkv, 1))
+        sq = rng.uniform(lo, hi, hq).astype(np.float32)
+        sk = rng.uniform(lo, hi, hkv).astype(np.float32)
+        sv = rng.uniform(lo, hi, hkv).astype(np.float32)
+        q *= sq.reshape(1, hq, 1)
+        k *= sk.reshape(1, hkv, 1)
+        v *= sv.reshape(1, hkv, 1)
     if key0_boost is not None and total > 0:
-        k[0].mul_(float(key0_boost))
-    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+        k[0] *= np.float32(key0_boost)
+    return tuple(torch.from_numpy(x).to(torch.bfloat16) for x in (q, k, v))
 
 
 def workload_qkv(w: Workload, layer: int = 0):
