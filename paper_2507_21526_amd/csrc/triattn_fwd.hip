@@ -24,6 +24,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "triattn_internal.h"
 
@@ -116,24 +117,65 @@ __device__ __forceinline__ float pair_sum(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Running maxima are re-based lazily: the output accumulator is rescaled only
+// when a row maximum grows by more than this many powers of two, so
+// probabilities stay below 2^kRescaleLog2 relative to the stale maximum.
+constexpr float kRescaleLog2 = 8.0f;
+
+// Register fences: an empty volatile asm that reads and rewrites a value, so
+// the computation producing it cannot be moved past this point (side-effect
+// free arithmetic could otherwise be sunk across a phase boundary).
+__device__ __forceinline__ void fence_regs(f32x16 &x)
+{
+    asm volatile("" : "+v"(x));
+}
+__device__ __forceinline__ void fence_regs(bf16x8 &x)
+{
+    asm volatile("" : "+v"(x));
+}
+__device__ __forceinline__ void fence_regs(float &x)
+{
+    asm volatile("" : "+v"(x));
+}
+
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// LDS tiles hold 64 keys x D in the natural [key][d] order, rows of 2D bytes,
+// with the 16-byte chunks of row r permuted by an XOR swizzle so that the
+// MFMA operand reads are free of bank conflicts:
+//   K (ds_read_b128 of 16 rows at one chunk): chunk' = chunk ^ kswz(r)
+//   V (transposed ds_read_b64_tr_b16 of 4 rows x 4 chunks per 32 lanes):
+//     chunk' = chunk ^ vswz(r)
+template <int D>
+__device__ __forceinline__ int kswz(int r)
+{
+    return D == 128 ? (r & 15) : ((r >> 1) & 7);
+}
+template <int D>
+__device__ __forceinline__ int vswz(int r)
+{
+    return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
+}
+
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t kind)
 {
-    constexpr int NT = NW * 64;
-    constexpr int KS = D + 8;      // K row stride in LDS (bf16 elements)
-    constexpr int VS = kStep + 8;  // V^T row stride in LDS (bf16 elements)
-    constexpr int K_ELEMS = kStep * KS;
-    constexpr int V_ELEMS = D * VS;
-    constexpr int STAGE = K_ELEMS + V_ELEMS;
-    constexpr int DCH = D / 8;                     // 16-byte chunks per row
-    constexpr int K_CHUNKS = kStep * DCH;          // K tile chunks
-    constexpr int V_CHUNKS = (kStep / 2) * DCH;    // V tile key-pair chunks
-    constexpr int K_LOADS = (K_CHUNKS + NT - 1) / NT;
-    constexpr int V_LOADS = (V_CHUNKS + NT - 1) / NT;
+    constexpr int ROW_BYTES = 2 * D;
+    constexpr int CHUNKS = D / 8;                       // 16-byte chunks per row
+    constexpr int TILE_BYTES = kStep * ROW_BYTES;       // one K or V tile
+    constexpr int STAGE_BYTES = 2 * TILE_BYTES;         // K tile, then V tile
+    constexpr int ROWS_PER_DMA = 1024 / ROW_BYTES;      // rows per wave DMA
+    constexpr int N_DMA = kStep / ROWS_PER_DMA;         // wave DMAs per tile
+    constexpr int DMA_PER_WAVE = (N_DMA + NW - 1) / NW;
     constexpr int QK_STEPS = D / 16;
     constexpr int D_BLOCKS = D / 32;
 
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * STAGE];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE_BYTES];
 
     const int32_t *sched = a.sched;
     if (!header_ok(sched, a.total_tokens, a.n_items, kind))
@@ -167,7 +209,10 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // The wave index is the same on every lane; reading it from lane 0 makes
+    // everything derived from it (head, rows, ping-pong group) scalar, so the
+    // per-wave branches below are uniform.
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = lane >> 5;
     const int col = lane & 31;
     const int waves_per_head = a.rows_per_wg / 32;
@@ -178,6 +223,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const bool row_valid = my_row < r1;
     const int load_row = row_valid ? my_row : r1 - 1;
     const int row_hi = (r1 - 1 < row_base + 31) ? r1 - 1 : row_base + 31;
+    const float c = a.scale_log2;
 
     // Steps of 64 keys over the kept k-tiles.
     const int tps = a.tile / kStep;
@@ -199,193 +245,281 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
 
     const uint16_t *kbase = a.k + (seq_off * a.hkv + g) * (int64_t)D;
     const uint16_t *vbase = a.v + (seq_off * a.hkv + g) * (int64_t)D;
-    const int64_t tok_stride = (int64_t)a.hkv * D;
+    const int tok_stride = a.hkv * D;
 
-    u32x4 kreg[K_LOADS];
-    u32x4 vreg[V_LOADS][2];
-
-    auto load_tile = [&](int key0) {
+    // Global -> LDS copies: wave DMA number m writes 1 KB = ROWS_PER_DMA rows
+    // of a tile; lane l lands at byte 16 l of it, i.e. row m*ROWS_PER_DMA +
+    // l / CHUNKS, stored chunk l % CHUNKS, which holds logical chunk
+    // (l % CHUNKS) ^ swizzle(row).
+    const int dma_row_in = lane / CHUNKS;
+    const int dma_pc = lane % CHUNKS;
+    int k_off[DMA_PER_WAVE], v_off[DMA_PER_WAVE];  // element offsets in a step
 #pragma unroll
-        for (int i = 0; i < K_LOADS; ++i) {
-            const int c = tid + i * NT;
-            if (c < K_CHUNKS) {
-                const int key = key0 + c / DCH;
-                const int dc = c % DCH;
-                if (key < seq_len)
-                    kreg[i] = *reinterpret_cast<const u32x4 *>(
-                        kbase + key * tok_stride + dc * 8);
-                else
-                    kreg[i] = u32x4{0, 0, 0, 0};
-            }
-        }
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+        const int m = wave + i * NW;
+        const int r = m * ROWS_PER_DMA + dma_row_in;
+        k_off[i] = r * tok_stride + (dma_pc ^ kswz<D>(r)) * 8;
+        v_off[i] = r * tok_stride + (dma_pc ^ vswz<D>(r)) * 8;
+    }
+    // Keys past the end of the sequence are read from its last row: they lie
+    // beyond every row of the item, so the causal mask gives them p = 0.
+    const int key_max = seq_len - 1;
+    auto dma_step = [&](int key0, int buf, bool do_k, bool do_v) {
+        unsigned char *stage = smem + buf * STAGE_BYTES;
+        const bool whole = key0 + kStep <= seq_len;
 #pragma unroll
-        for (int i = 0; i < V_LOADS; ++i) {
-            const int c = tid + i * NT;
-            if (c < V_CHUNKS) {
-                const int kp = c % (kStep / 2);
-                const int dc = c / (kStep / 2);
-                const int key = key0 + 2 * kp;
-#pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    if (key + e < seq_len)
-                        vreg[i][e] = *reinterpret_cast<const u32x4 *>(
-                            vbase + (key + e) * tok_stride + dc * 8);
-                    else
-                        vreg[i][e] = u32x4{0, 0, 0, 0};
+        for (int i = 0; i < DMA_PER_WAVE; ++i) {
+            const int m = wave + i * NW;
+            if (m < N_DMA) {
+                int ko = k_off[i], vo = v_off[i];
+                if (!whole) {
+                    const int r = m * ROWS_PER_DMA + dma_row_in;
+                    const int kr = min(key0 + r, key_max) - key0;
+                    ko = kr * tok_stride + (dma_pc ^ kswz<D>(r)) * 8;
+                    vo = kr * tok_stride + (dma_pc ^ vswz<D>(r)) * 8;
                 }
+                const int64_t step = (int64_t)key0 * tok_stride;
+                if (do_k)
+                    __builtin_amdgcn_global_load_lds(
+                        kbase + step + ko,
+                        (__attribute__((address_space(3))) void *)(stage + m * 1024), 16, 0, 0);
+                if (do_v)
+                    __builtin_amdgcn_global_load_lds(
+                        vbase + step + vo,
+                        (__attribute__((address_space(3))) void *)(stage + TILE_BYTES + m * 1024),
+                        16, 0, 0);
             }
         }
     };
 
-    auto store_tile = [&](int buf) {
-        uint16_t *kl = smem + buf * STAGE;
-        uint32_t *vl = reinterpret_cast<uint32_t *>(kl + K_ELEMS);
+    // S^T = K Q^T for one 64-key step from LDS stage `buf`; the two 32-key
+    // accumulator chains alternate so that dependent MFMAs do not stall.
+    const int krow0 = perm_row(col), krow1 = 32 + perm_row(col);
+    auto qk = [&](int buf, f32x16 (&sacc)[2]) {
+        const unsigned char *kt = smem + buf * STAGE_BYTES;
+        sacc[0] = f32x16{};
+        sacc[1] = f32x16{};
 #pragma unroll
-        for (int i = 0; i < K_LOADS; ++i) {
-            const int c = tid + i * NT;
-            if (c < K_CHUNKS) {
-                const int key = c / DCH, dc = c % DCH;
-                *reinterpret_cast<u32x4 *>(kl + key * KS + dc * 8) = kreg[i];
-            }
+        for (int s = 0; s < QK_STEPS; ++s) {
+            const int ch = 2 * s + half;
+            const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(
+                kt + krow0 * ROW_BYTES + ((ch ^ kswz<D>(krow0)) << 4));
+            const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(
+                kt + krow1 * ROW_BYTES + ((ch ^ kswz<D>(krow1)) << 4));
+            sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], sacc[0], 0, 0, 0);
+            sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], sacc[1], 0, 0, 0);
         }
+        // keep six operand reads in flight ahead of the MFMAs
+        constexpr int n = 2 * QK_STEPS, ahead = 6;
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
 #pragma unroll
-        for (int i = 0; i < V_LOADS; ++i) {
-            const int c = tid + i * NT;
-            if (c < V_CHUNKS) {
-                const int kp = c % (kStep / 2);
-                const int dc = c / (kStep / 2);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    // element e of each key's chunk: pack (key 2kp, key 2kp+1)
-                    const uint32_t lo = (vreg[i][0][e >> 1] >> (16 * (e & 1))) & 0xffffu;
-                    const uint32_t hi = (vreg[i][1][e >> 1] >> (16 * (e & 1))) & 0xffffu;
-                    vl[((dc * 8 + e) * VS) / 2 + kp] = lo | (hi << 16);
-                }
-            }
+        for (int i = 0; i < n - ahead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
         }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
     };
 
     f32x16 oacc[D_BLOCKS];
 #pragma unroll
     for (int b = 0; b < D_BLOCKS; ++b)
         oacc[b] = f32x16{};
-    float m_run = -INFINITY;  // running max, log2 domain (scaled)
-    float l_run = 0.f;        // running sum, this lane's keys only
 
-    if (nsteps > 0) {
-        load_tile(step_key0(0));
-        store_tile(0);
-    }
-    __syncthreads();
-
-    for (int st = 0; st < nsteps; ++st) {
-        const int buf = st & 1;
-        const int key0 = step_key0(st);
-        const bool more = st + 1 < nsteps;
-        if (more)
-            load_tile(step_key0(st + 1));
-
-        // Is any (row, key) pair of this wave kept in this step?
-        bool any = wave_active && key0 <= row_hi;
-        if (any && mode == kModeStreaming)
-            any = (key0 < a.sink) || (row_base - (key0 + kStep - 1) < a.window);
-        if (any) {
-            const uint16_t *kl = smem + buf * STAGE;
-            const uint16_t *vl = kl + K_ELEMS;
-            f32x16 sacc[2];
+    // O^T += V^T P^T for one 64-key step from LDS stage `buf`.  The V^T
+    // fragment of 8 keys x 1 d comes from two transposed reads: in each group
+    // of 16 lanes, lane i addresses row K0 + i/4 at d = D0 + 4 (i % 4), and
+    // lane j receives rows K0..K0+3 at d = D0 + j.
+    const int tr_row = (lane & 15) >> 2;                       // + K0
+    const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);  // + 32 b
+    auto pv = [&](int buf, const bf16x8 (&pf)[2][2]) {
+        const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                sacc[kb] = f32x16{};
-                const uint16_t *kr = kl + (kb * 32 + perm_row(col)) * KS + 8 * half;
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int s = 0; s < QK_STEPS; ++s) {
-                    const bf16x8 af = *reinterpret_cast<const bf16x8 *>(kr + 16 * s);
-                    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[s],
-                                                                      sacc[kb], 0, 0, 0);
-                }
-            }
-
-            // Element mask where the step crosses the diagonal or the window.
-            const bool need_mask =
-                (key0 + kStep - 1 > row_base) ||
-                (mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
-                 row_hi - key0 >= a.window);
-            if (need_mask) {
+            for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+                for (int b = 0; b < D_BLOCKS; ++b) {
+                    s16x4 part[2];
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int key = key0 + kb * 32 + key_of_reg(v, half);
-                        bool keep = key <= my_row;
-                        if (mode == kModeStreaming)
-                            keep = keep && (key < a.sink || my_row - key < a.window);
-                        if (!keep)
-                            sacc[kb][v] = -INFINITY;
+                    for (int i2 = 0; i2 < 2; ++i2) {
+                        const int r = kb * 32 + s2 * 16 + 8 * half + 4 * i2 + tr_row;
+                        const int d = 32 * b + tr_d;
+                        const int off = r * ROW_BYTES + (((d >> 3) ^ vswz<D>(r)) << 4) +
+                                        (d & 7) * 2;
+                        part[i2] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4 *)(vt + off));
                     }
-            }
-
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    mx = fmaxf(mx, sacc[kb][v]);
-            mx = pair_max(mx);
-            const float m_new = fmaxf(m_run, mx * a.scale_log2);
-            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-            m_run = m_new;
-
-            float psum = 0.f;
-            bf16x8 pf[2][2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const float p = __builtin_amdgcn_exp2f(
-                        __builtin_fmaf(sacc[kb][v], a.scale_log2, -m_use));
-                    sacc[kb][v] = p;
-                    psum += p;
+                    const bf16x8 af = __builtin_bit_cast(
+                        bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5,
+                                                        6, 7));
+                    oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[kb][s2],
+                                                                     oacc[b], 0, 0, 0);
                 }
+        // two transposed reads per MFMA; keep four MFMAs' operands in flight
+        constexpr int n = 4 * D_BLOCKS, ahead = 4;
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * ahead, 0);
 #pragma unroll
-                for (int s2 = 0; s2 < 2; ++s2) {
-                    f32x8 t;
+        for (int i = 0; i < n - ahead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
+    };
+
+    // Element mask (branch-free selects) where the step crosses the diagonal
+    // or the window edge; keys beyond the sequence are beyond every row.
+    auto mask_step = [&](int key0, f32x16 (&sacc)[2]) {
+        const int lim = my_row - key0 - 8 * half;        // key offset <= lim
+        // streaming rows also need offset < sink_lim or offset > win_lim
+        const bool stream_mode = mode == kModeStreaming;
+        const int sink_lim = stream_mode ? a.sink - key0 - 8 * half : kStep;
+        const int win_lim = stream_mode ? lim - a.window : -1;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        t[e] = sacc[kb][8 * s2 + e];
-                    pf[kb][s2] = __builtin_convertvector(t, bf16x8);
-                }
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int off = kb * 32 + (v & 7) + 16 * (v >> 3);
+                const bool keep = (off <= lim) & ((off < sink_lim) | (off > win_lim));
+                sacc[kb][v] = keep ? sacc[kb][v] : -INFINITY;
             }
-            l_run = l_run * alpha + psum;
+    };
+    auto step_needs_mask = [&](int key0) -> bool {
+        return (key0 + kStep - 1 > row_base) ||
+               (mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
+                row_hi - key0 >= a.window);
+    };
+
+    float m_ref = -INFINITY;  // reference maximum of the row, log2 domain
+    float l_run = 0.f;        // running sum over this lane's keys
+
+    // Online softmax of one step: probabilities relative to the (lazily
+    // re-based) reference maximum, converted to the bf16 B operand of PV.
+    // O holds every earlier step already, so a re-base rescales it here.
+    auto softmax = [&](f32x16 (&sacc)[2], bf16x8 (&pf)[2][2]) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                mx = fmaxf(mx, sacc[kb][v]);
+        mx = pair_max(mx);
+        const float m_new = fmaxf(m_ref, mx * c);
+        const bool need = __builtin_amdgcn_ballot_w64(m_new > m_ref + kRescaleLog2) != 0;
+        const float m_upd = need ? m_new : m_ref;
+        const float m_use = (m_upd == -INFINITY) ? 0.f : m_upd;
+        if (need) {
+            const float alpha = __builtin_amdgcn_exp2f(m_ref - m_use);
+            l_run *= alpha;
 #pragma unroll
             for (int b = 0; b < D_BLOCKS; ++b)
                 oacc[b] *= alpha;
+        }
+        m_ref = m_upd;
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+                f32x8 t;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    t[e] = __builtin_amdgcn_exp2f(
+                        __builtin_fmaf(sacc[kb][8 * s2 + e], c, -m_use));
+                    psum += t[e];
+                }
+                pf[kb][s2] = __builtin_convertvector(t, bf16x8);
+            }
+        l_run += psum;
+    };
 
+    // Two-group ping-pong.  The waves are split into two groups with one wave
+    // of each group on every SIMD.  Work of a wave, in order: M(0), X(0),
+    // M(1), X(1), ..., M(n), where M(j) = { S(j) = K(j) Q^T ; O += V(j-1)
+    // P(j-1) } runs on the matrix cores and X(j) = softmax of S(j) runs on
+    // the vector units.  Group 0 runs M(j) in phase 2j and X(j) in phase
+    // 2j + 1; group 1 runs X(j-1) in phase 2j and M(j) in phase 2j + 1, so in
+    // every phase one wave of each SIMD issues MFMAs while the other issues
+    // the softmax.  LDS stage j&1 holds K(j) and V(j-1) during phases 2j and
+    // 2j+1; K(j+1) and V(j) are copied into stage (j+1)&1 from the start of
+    // phase 2j and are complete at the barrier that ends phase 2j+1.
+    const int n_group1 = NW / 2;
+    const int group = NW >= 2 ? (wave >= NW - n_group1 ? 1 : 0) : 0;
+    f32x16 s_acc[2];
+    bf16x8 p_acc[2][2];
+
+    auto do_m = [&](int j) {
+        const int buf = j & 1;
+        if (j < nsteps) {
+            qk(buf, s_acc);
+            fence_regs(s_acc[0]);
+            fence_regs(s_acc[1]);
+        }
+        if (j >= 1) {
+            pv(buf, p_acc);
 #pragma unroll
-            for (int b = 0; b < D_BLOCKS; ++b) {
-                const uint16_t *vr = vl + (b * 32 + col) * VS + 8 * half;
+            for (int b = 0; b < D_BLOCKS; ++b)
+                fence_regs(oacc[b]);
+        }
+    };
+    auto do_x = [&](int j) {
+        const int key0 = step_key0(j);
+        if (step_needs_mask(key0))
+            mask_step(key0, s_acc);
+        softmax(s_acc, p_acc);
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                    for (int s2 = 0; s2 < 2; ++s2) {
-                        const bf16x8 af = *reinterpret_cast<const bf16x8 *>(
-                            vr + kb * 32 + s2 * 16);
-                        oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            af, pf[kb][s2], oacc[b], 0, 0, 0);
-                    }
+            for (int s2 = 0; s2 < 2; ++s2)
+                fence_regs(p_acc[kb][s2]);
+        fence_regs(l_run);
+        fence_regs(m_ref);
+    };
+    auto fetch = [&](int j) {
+        const bool k_next = j + 1 < nsteps, v_cur = j < nsteps;
+        if (k_next)
+            dma_step(step_key0(j + 1), (j + 1) & 1, true, false);
+        if (v_cur)
+            dma_step(step_key0(j), (j + 1) & 1, false, true);
+    };
+    // A phase boundary: the scheduler may not move any instruction across it
+    // (MFMAs and VALU work must stay in their own phase).
+    auto end_phase = [&](bool wait_dma) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (wait_dma)
+            __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's copies landed
+        __syncthreads();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    if (nsteps > 0) {
+        dma_step(step_key0(0), 0, true, false);
+        end_phase(true);
+        if (group == 0) {
+            for (int j = 0; j <= nsteps; ++j) {
+                fetch(j);
+                do_m(j);
+                end_phase(false);
+                if (j < nsteps)
+                    do_x(j);
+                end_phase(true);
+            }
+        } else {
+            for (int j = 0; j <= nsteps; ++j) {
+                fetch(j);
+                if (j >= 1)
+                    do_x(j - 1);
+                end_phase(false);
+                do_m(j);
+                end_phase(true);
             }
         }
-
-        if (more)
-            store_tile(buf ^ 1);
-        __syncthreads();
     }
 
     if (!wave_active)
         return;
     const float l_tot = pair_sum(l_run);
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-    const float row_lse = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    const float row_lse = l_tot > 0.f ? (m_ref + __log2f(l_tot)) * kLn2 : -INFINITY;
     if (!row_valid)
         return;
 
@@ -546,9 +680,7 @@ template <int D>
 hipError_t launch_tile(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_t s)
 {
     switch (nw) {
-    case 1: hipLaunchKernelGGL((attn_tile_kernel<D, 1>), grid, dim3(64), 0, s, a, kind); break;
     case 2: hipLaunchKernelGGL((attn_tile_kernel<D, 2>), grid, dim3(128), 0, s, a, kind); break;
-    case 3: hipLaunchKernelGGL((attn_tile_kernel<D, 3>), grid, dim3(192), 0, s, a, kind); break;
     case 4: hipLaunchKernelGGL((attn_tile_kernel<D, 4>), grid, dim3(256), 0, s, a, kind); break;
     case 5: hipLaunchKernelGGL((attn_tile_kernel<D, 5>), grid, dim3(320), 0, s, a, kind); break;
     case 6: hipLaunchKernelGGL((attn_tile_kernel<D, 6>), grid, dim3(384), 0, s, a, kind); break;

@@ -66,8 +66,15 @@ def sample_rows(cu, sink, window, last, tile, n_random, seed, all_last=True):
     return np.array(sorted(toks), dtype=np.int64)
 
 
+def bf16_p_bound(v_cpu):
+    """Largest output error the bf16 rounding of the probabilities can cause:
+    |sum_j dp_j v_j| / sum_j p_j <= 2^-8 max_j |v_j| (round-to-nearest bf16
+    has relative error <= 2^-8).  Rows with few keys can reach it."""
+    return 2.0 ** -8 * float(v_cpu.float().abs().max())
+
+
 def compare(kind, q_cpu, k_cpu, v_cpu, cu, sink, window, last, scale, o, lse,
-            toks, heads, label=""):
+            toks, heads, label="", max_abs=MAX_ABS):
     """Check GPU rows o[toks, h] (fp32/bf16 cuda) against the oracle."""
     toks = np.asarray(toks, dtype=np.int64)
     heads = list(heads)
@@ -83,15 +90,15 @@ def compare(kind, q_cpu, k_cpu, v_cpu, cu, sink, window, last, scale, o, lse,
     for h in heads:
         sel = rh == h
         err = got_o[sel] - ref_o[sel]
-        max_abs = float(np.abs(err).max()) if err.size else 0.0
+        max_err = float(np.abs(err).max()) if err.size else 0.0
         rel = float(np.linalg.norm(err) / max(np.linalg.norm(ref_o[sel]), 1e-30))
         lse_err = float(np.abs(got_lse[sel] - ref_lse[sel]).max())
-        worst[h] = (max_abs, rel, lse_err)
-        if not (max_abs <= MAX_ABS and rel <= REL_L2 and lse_err <= LSE_ABS):
-            bad = np.argwhere(np.abs(err) > MAX_ABS)
+        worst[h] = (max_err, rel, lse_err)
+        if not (max_err <= max_abs and rel <= REL_L2 and lse_err <= LSE_ABS):
+            bad = np.argwhere(np.abs(err) > max_abs)
             rows = sorted(set(int(rt[sel][i]) for i, _ in bad[:20]))
             raise AssertionError(
-                f"{label} head {h}: max-abs {max_abs:.3e}, rel-L2 {rel:.3e}, "
+                f"{label} head {h}: max-abs {max_err:.3e}, rel-L2 {rel:.3e}, "
                 f"lse {lse_err:.3e}; first bad tokens {rows[:10]}")
     log(f"{label}: {len(toks)} rows x {len(heads)} heads, worst max-abs "
         f"{max(w[0] for w in worst.values()):.2e} rel-L2 "
