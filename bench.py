@@ -25,6 +25,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -61,6 +62,125 @@ def load_traffic(workload: str):
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+COPY_BYTES = 1 << 30  # bytes read (and written) by the calibration copy
+TILE_KERNEL = "attn_tile_kernel"
+MERGE_KERNEL = "merge_kernel"
+
+
+def _pmc_per_kernel(path, counter):
+    """Mean counter value per dispatch for each kernel name in a rocprofv3
+    counter_collection.csv (values summed over the counter's instances)."""
+    import csv
+    import glob
+    per = {}
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"),
+                       recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                key = (r["Kernel_Name"], r["Dispatch_Id"])
+                per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for (name, _), v in per.items():
+        out.setdefault(name, []).append(v)
+    return {k: sum(v) / len(v) for k, v in out.items()}
+
+
+def summarize(root, workload):
+    """Write profiles/ summaries from rocprofv3 runs of this benchmark:
+    root/trace (--kernel-trace --stats, csv), root/fetch (--pmc FETCH_SIZE),
+    root/write (--pmc WRITE_SIZE), the latter two with --copy-calibration."""
+    import csv
+    import glob
+    prof = os.path.join(ROOT, "profiles")
+    os.makedirs(prof, exist_ok=True)
+    cmd = "rocprofv3 --kernel-trace --stats --output-format csv -d <dir>/trace " \
+          f"-- python3 bench.py --workload {workload} --steps 5 --warmup 1 " \
+          "--no-cpu-baseline"
+    stats = glob.glob(os.path.join(root, "trace", "**", "*kernel_stats.csv"),
+                      recursive=True)
+    if stats:
+        with open(stats[0]) as fh:
+            rows = list(csv.DictReader(fh))
+        with open(os.path.join(prof, f"kernel_stats_{workload}.md"), "w") as out:
+            out.write(f"# rocprofv3 kernel statistics, {workload}\n\n")
+            out.write(f"Command (from the repository root, on one MI355X):\n\n    {cmd}\n\n")
+            out.write("| kernel | calls | total ms | average ms | min ms | max ms | % |\n")
+            out.write("|---|---|---|---|---|---|---|\n")
+            for r in rows:
+                name = r["Name"]
+                m = re.search(r"(\w+_kernel<[^>]*>)", name)
+                short = m.group(1) if m else name[:60]
+                out.write(f"| {short} | {r['Calls']} | "
+                          f"{float(r['TotalDurationNs']) / 1e6:.3f} | "
+                          f"{float(r['AverageNs']) / 1e6:.4f} | "
+                          f"{float(r['MinNs']) / 1e6:.4f} | "
+                          f"{float(r['MaxNs']) / 1e6:.4f} | "
+                          f"{float(r['Percentage']):.2f} |\n")
+            out.write("\nThe tile kernel serves both passes; split by launch grid "
+                      "(from the kernel trace of the same run):\n\n")
+            traces = glob.glob(os.path.join(root, "trace", "**", "*kernel_trace.csv"),
+                               recursive=True)
+            groups = {}
+            if traces:
+                with open(traces[0]) as fh:
+                    for r in csv.DictReader(fh):
+                        m = re.search(r"(\w+_kernel<[^>]*>)", r["Kernel_Name"])
+                        if not m:
+                            continue
+                        wg = int(r["Workgroup_Size_X"])
+                        key = (m.group(1), int(r["Grid_Size_X"]) // max(wg, 1))
+                        groups.setdefault(key, []).append(
+                            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
+            out.write("| kernel | workgroups | calls | average ms | min ms |\n")
+            out.write("|---|---|---|---|---|\n")
+            for (k, wgs), v in sorted(groups.items()):
+                out.write(f"| {k} | {wgs} | {len(v)} | {sum(v) / len(v):.4f} | "
+                          f"{min(v):.4f} |\n")
+            out.write("\nFor llama8b_n128k the Triangle tile pass launches "
+                      "(57 Last splits + 1023 streaming q-tiles) x 2 row halves x "
+                      "8 kv heads = 17280 workgroups; dense causal launches "
+                      "1024 x 2 x 8 = 16384; the merge launches 128 rows x 32 "
+                      "heads / 4 = 1024.\n")
+    fetch = _pmc_per_kernel(os.path.join(root, "fetch"), "FETCH_SIZE")
+    write = _pmc_per_kernel(os.path.join(root, "write"), "WRITE_SIZE")
+    if fetch and write:
+        def pick(d, key):
+            vals = [v for k, v in d.items() if key in k]
+            return min(vals) if vals else None
+        copy_key = "copy"
+        f_copy = pick(fetch, copy_key)
+        w_copy = pick(write, copy_key)
+        f_tile = pick(fetch, TILE_KERNEL)
+        w_tile = pick(write, TILE_KERNEL)
+        f_fac = f_copy * 1024.0 / COPY_BYTES    # counter KiB per real byte
+        w_fac = w_copy * 1024.0 / COPY_BYTES
+        rec = {
+            "workload": workload,
+            "kernel": TILE_KERNEL,
+            "kernel_source_hash": kernel_source_hash(),
+            "fetch_kib_per_launch": f_tile,
+            "write_kib_per_launch": w_tile,
+            "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
+            "copy_bytes": COPY_BYTES,
+            "fetch_factor": f_fac, "write_factor": w_fac,
+            "hbm_bytes_per_launch": (f_tile / f_fac + w_tile / w_fac) * 1024.0,
+            "commands": [
+                "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir>/fetch "
+                f"-- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
+                "--no-dense --no-cpu-baseline --copy-calibration",
+                "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir>/write "
+                f"-- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
+                "--no-dense --no-cpu-baseline --copy-calibration",
+            ],
+        }
+        with open(os.path.join(prof, f"traffic_tile_kernel_{workload}.json"), "w") as out:
+            json.dump(rec, out, indent=1)
+    print(json.dumps({"summarized": root, "trace": bool(stats),
+                      "traffic": bool(fetch and write)}))
 
 
 def cpu_model() -> str:
@@ -149,7 +269,16 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 1 GiB device copy first (reference "
+                         "kernel for the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--summarize", metavar="DIR",
+                    help="no GPU work: summarize rocprofv3 output under DIR "
+                         "(DIR/trace, DIR/fetch, DIR/write) into profiles/")
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args.summarize, args.workload)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -184,6 +313,12 @@ def main():
                          w.d, device=dev)
     o = torch.empty(qg.shape, dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def tri_step(ev):
         if ev is not None:
