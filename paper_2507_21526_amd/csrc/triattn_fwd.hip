@@ -138,6 +138,52 @@ __device__ __forceinline__ void fence_regs(float &x)
     asm volatile("" : "+v"(x));
 }
 
+// One wave-wide 16-byte-per-lane copy from global memory straight into LDS
+// (lane l lands at lds_addr + 16 l).  Issued from inline assembly so that the
+// compiler does not serialise it against unrelated LDS reads (the copy
+// targets the other LDS stage; barriers order it against the readers of its
+// own stage): completion is tracked explicitly with vmcnt waits.  M0 holds
+// the LDS address during the copy and is restored afterwards.
+__device__ __forceinline__ void copy_to_lds16(const void *gbase, uint32_t lane_byte_off,
+                                              uint32_t lds_addr)
+{
+    uint32_t saved;
+    asm volatile("s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %1\n\t"
+                 "s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %2, %3\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(lds_addr), "v"(lane_byte_off), "s"(gbase));
+}
+
+// Workgroup barrier without a memory fence: this wave's LDS reads are
+// complete (lgkmcnt 0); copies into LDS are synchronised by vmcnt waits.
+__device__ __forceinline__ void barrier_no_fence()
+{
+    asm volatile("" ::: "memory");       // no compiler motion of memory ops
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// s_waitcnt vmcnt(n) for a run-time n (small): the count is an immediate.
+__device__ __forceinline__ void wait_vmcnt(int n)
+{
+    // expcnt and lgkmcnt fields left at their maximum (no wait on them)
+    switch (n) {
+    case 0: __builtin_amdgcn_s_waitcnt(0x0f70); break;
+    case 1: __builtin_amdgcn_s_waitcnt(0x0f71); break;
+    case 2: __builtin_amdgcn_s_waitcnt(0x0f72); break;
+    case 3: __builtin_amdgcn_s_waitcnt(0x0f73); break;
+    case 4: __builtin_amdgcn_s_waitcnt(0x0f74); break;
+    case 5: __builtin_amdgcn_s_waitcnt(0x0f75); break;
+    case 6: __builtin_amdgcn_s_waitcnt(0x0f76); break;
+    case 7: __builtin_amdgcn_s_waitcnt(0x0f77); break;
+    default: __builtin_amdgcn_s_waitcnt(0x0f78); break;
+    }
+}
+
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
 constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
@@ -169,13 +215,20 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     constexpr int CHUNKS = D / 8;                       // 16-byte chunks per row
     constexpr int TILE_BYTES = kStep * ROW_BYTES;       // one K or V tile
     constexpr int STAGE_BYTES = 2 * TILE_BYTES;         // K tile, then V tile
-    constexpr int ROWS_PER_DMA = 1024 / ROW_BYTES;      // rows per wave DMA
-    constexpr int N_DMA = kStep / ROWS_PER_DMA;         // wave DMAs per tile
-    constexpr int DMA_PER_WAVE = (N_DMA + NW - 1) / NW;
+    constexpr int N_STAGES = 2;                         // LDS double buffer
+    constexpr int ROWS_PER_DMA = 1024 / ROW_BYTES;      // rows per wave copy
+    constexpr int N_DMA = kStep / ROWS_PER_DMA;         // wave copies per tile
+    // Only the waves of ping-pong group 0 copy K/V tiles into LDS, spread
+    // over the MFMAs of their matrix phase (see the phase loop below).
+    constexpr int N_COPY_WAVES = NW - NW / 2;
+    constexpr int COPIES = (N_DMA + N_COPY_WAVES - 1) / N_COPY_WAVES;  // per tile
     constexpr int QK_STEPS = D / 16;
     constexpr int D_BLOCKS = D / 32;
+    constexpr int MFMA_SLOTS = 2 * QK_STEPS + 4 * D_BLOCKS;  // MFMAs of a matrix phase
+    constexpr int COPY_STRIDE = MFMA_SLOTS / (2 * COPIES) > 0
+                                    ? MFMA_SLOTS / (2 * COPIES) : 1;
 
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[N_STAGES * STAGE_BYTES];
 
     const int32_t *sched = a.sched;
     if (!header_ok(sched, a.total_tokens, a.n_items, kind))
@@ -247,55 +300,69 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const uint16_t *vbase = a.v + (seq_off * a.hkv + g) * (int64_t)D;
     const int tok_stride = a.hkv * D;
 
-    // Global -> LDS copies: wave DMA number m writes 1 KB = ROWS_PER_DMA rows
-    // of a tile; lane l lands at byte 16 l of it, i.e. row m*ROWS_PER_DMA +
+    // Global -> LDS copies: copy number m of a tile writes 1 KB = ROWS_PER_DMA
+    // rows; lane l lands at byte 16 l of it, i.e. row m*ROWS_PER_DMA +
     // l / CHUNKS, stored chunk l % CHUNKS, which holds logical chunk
-    // (l % CHUNKS) ^ swizzle(row).
+    // (l % CHUNKS) ^ swizzle(row).  Copy waves (group 0, wave w < N_COPY_WAVES)
+    // own copies m = w, w + N_COPY_WAVES, ... of every K and V tile.
+    const bool copy_wave = wave < N_COPY_WAVES;
     const int dma_row_in = lane / CHUNKS;
     const int dma_pc = lane % CHUNKS;
-    int k_off[DMA_PER_WAVE], v_off[DMA_PER_WAVE];  // element offsets in a step
-#pragma unroll
-    for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const int m = wave + i * NW;
-        const int r = m * ROWS_PER_DMA + dma_row_in;
-        k_off[i] = r * tok_stride + (dma_pc ^ kswz<D>(r)) * 8;
-        v_off[i] = r * tok_stride + (dma_pc ^ vswz<D>(r)) * 8;
-    }
     // Keys past the end of the sequence are read from its last row: they lie
     // beyond every row of the item, so the causal mask gives them p = 0.
     const int key_max = seq_len - 1;
-    auto dma_step = [&](int key0, int buf, bool do_k, bool do_v) {
-        unsigned char *stage = smem + buf * STAGE_BYTES;
-        const bool whole = key0 + kStep <= seq_len;
-#pragma unroll
-        for (int i = 0; i < DMA_PER_WAVE; ++i) {
-            const int m = wave + i * NW;
-            if (m < N_DMA) {
-                int ko = k_off[i], vo = v_off[i];
-                if (!whole) {
-                    const int r = m * ROWS_PER_DMA + dma_row_in;
-                    const int kr = min(key0 + r, key_max) - key0;
-                    ko = kr * tok_stride + (dma_pc ^ kswz<D>(r)) * 8;
-                    vo = kr * tok_stride + (dma_pc ^ vswz<D>(r)) * 8;
-                }
-                const int64_t step = (int64_t)key0 * tok_stride;
-                if (do_k)
-                    __builtin_amdgcn_global_load_lds(
-                        kbase + step + ko,
-                        (__attribute__((address_space(3))) void *)(stage + m * 1024), 16, 0, 0);
-                if (do_v)
-                    __builtin_amdgcn_global_load_lds(
-                        vbase + step + vo,
-                        (__attribute__((address_space(3))) void *)(stage + TILE_BYTES + m * 1024),
-                        16, 0, 0);
-            }
-        }
+    const uint32_t smem_addr =
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+
+    // One tile copy (K or V of one step into one stage).  The lane offset of
+    // a copy is an unsigned 32-bit byte offset from a scalar base at key
+    // min(first key, last key of the sequence): row r of the tile reads key
+    // min(key0 + r, last key), so every offset is non-negative and below 64
+    // rows, and a step past the end of the sequence still reads valid rows.
+    struct TileCopy {
+        const uint16_t *base;
+        uint32_t lds;
+        int key0, key_base;
     };
+    auto plan_copy = [&](const uint16_t *src, int key0, int buf, bool is_v) -> TileCopy {
+        TileCopy t;
+        t.key0 = key0;
+        t.key_base = min(key0, key_max);
+        t.base = src + (int64_t)t.key_base * tok_stride;
+        t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0);
+        return t;
+    };
+    // Copy i of this wave (m = wave + i * N_COPY_WAVES) of a planned tile.
+    auto issue_copy = [&](const TileCopy &t, int i, bool is_v) {
+        const int m = wave + i * N_COPY_WAVES;
+        if constexpr (N_DMA % N_COPY_WAVES != 0) {
+            if (m >= N_DMA)
+                return;
+        }
+        const int r = m * ROWS_PER_DMA + dma_row_in;
+        const int kr = min(t.key0 + r, key_max) - t.key_base;  // in [0, 64)
+        const int off = kr * tok_stride + (dma_pc ^ (is_v ? vswz<D>(r) : kswz<D>(r))) * 8;
+        copy_to_lds16(t.base, 2u * (uint32_t)off, t.lds + m * 1024);
+    };
+    // Copy slot c (0 <= c < 2 * COPIES): K copies first, then V copies.
+    TileCopy cp_k{}, cp_v{};
+    auto issue_slot = [&](int c) {
+        if (c < COPIES)
+            issue_copy(cp_k, c, false);
+        else
+            issue_copy(cp_v, c - COPIES, true);
+    };
+    // Hook run after MFMA number `slot` of a matrix phase of a copy wave.
+    auto copy_hook = [&](int slot) {
+        if (slot % COPY_STRIDE == COPY_STRIDE - 1 && slot / COPY_STRIDE < 2 * COPIES)
+            issue_slot(slot / COPY_STRIDE);
+    };
+    auto no_hook = [](int) {};
 
     // S^T = K Q^T for one 64-key step from LDS stage `buf`; the two 32-key
     // accumulator chains alternate so that dependent MFMAs do not stall.
     const int krow0 = perm_row(col), krow1 = 32 + perm_row(col);
-    auto qk = [&](int buf, f32x16 (&sacc)[2]) {
+    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) {
         const unsigned char *kt = smem + buf * STAGE_BYTES;
         sacc[0] = f32x16{};
         sacc[1] = f32x16{};
@@ -307,7 +374,9 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
             const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(
                 kt + krow1 * ROW_BYTES + ((ch ^ kswz<D>(krow1)) << 4));
             sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], sacc[0], 0, 0, 0);
+            hook(2 * s);
             sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], sacc[1], 0, 0, 0);
+            hook(2 * s + 1);
         }
         // keep six operand reads in flight ahead of the MFMAs
         constexpr int n = 2 * QK_STEPS, ahead = 6;
@@ -331,7 +400,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     // lane j receives rows K0..K0+3 at d = D0 + j.
     const int tr_row = (lane & 15) >> 2;                       // + K0
     const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);  // + 32 b
-    auto pv = [&](int buf, const bf16x8 (&pf)[2][2]) {
+    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) {
         const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -354,6 +423,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
                                                         6, 7));
                     oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[kb][s2],
                                                                      oacc[b], 0, 0, 0);
+                    hook(2 * QK_STEPS + (kb * 2 + s2) * D_BLOCKS + b);
                 }
         // two transposed reads per MFMA; keep four MFMAs' operands in flight
         constexpr int n = 4 * D_BLOCKS, ahead = 4;
@@ -439,27 +509,29 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     // the vector units.  Group 0 runs M(j) in phase 2j and X(j) in phase
     // 2j + 1; group 1 runs X(j-1) in phase 2j and M(j) in phase 2j + 1, so in
     // every phase one wave of each SIMD issues MFMAs while the other issues
-    // the softmax.  LDS stage j&1 holds K(j) and V(j-1) during phases 2j and
-    // 2j+1; K(j+1) and V(j) are copied into stage (j+1)&1 from the start of
-    // phase 2j and are complete at the barrier that ends phase 2j+1.
+    // the softmax.  LDS stage j & 1 holds K(j) and V(j-1) for phases 2j and
+    // 2j+1.  During M(j) the group-0 waves copy K(j+1) and V(j) into stage
+    // (j+1) & 1 (last read in phase 2j-1), one copy after every COPY_STRIDE
+    // MFMAs so that the address units see a steady stream, and wait for them
+    // at the end of phase 2j+1.  The softmax waves issue no copies.
     const int n_group1 = NW / 2;
     const int group = NW >= 2 ? (wave >= NW - n_group1 ? 1 : 0) : 0;
     f32x16 s_acc[2];
     bf16x8 p_acc[2][2];
 
-    auto do_m = [&](int j) {
+    // Matrix phase: QK^T of step j (if any) and PV of step j-1 (if any).
+    auto do_m = [&](int j, bool has_qk, bool has_pv, auto hook) {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);  // MFMA issue goes first on the SIMD
+        __builtin_amdgcn_sched_barrier(0);
         const int buf = j & 1;
-        if (j < nsteps) {
-            qk(buf, s_acc);
-            fence_regs(s_acc[0]);
-            fence_regs(s_acc[1]);
-        }
-        if (j >= 1) {
-            pv(buf, p_acc);
-#pragma unroll
-            for (int b = 0; b < D_BLOCKS; ++b)
-                fence_regs(oacc[b]);
-        }
+        if (has_qk)
+            qk(buf, s_acc, hook);
+        if (has_pv)
+            pv(buf, p_acc, hook);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
     };
     auto do_x = [&](int j) {
         const int key0 = step_key0(j);
@@ -474,44 +546,66 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         fence_regs(l_run);
         fence_regs(m_ref);
     };
-    auto fetch = [&](int j) {
-        const bool k_next = j + 1 < nsteps, v_cur = j < nsteps;
-        if (k_next)
-            dma_step(step_key0(j + 1), (j + 1) & 1, true, false);
-        if (v_cur)
-            dma_step(step_key0(j), (j + 1) & 1, false, true);
-    };
     // A phase boundary: the scheduler may not move any instruction across it
     // (MFMAs and VALU work must stay in their own phase).
-    auto end_phase = [&](bool wait_dma) {
+    auto end_phase = [&](bool wait_copies) {
         __builtin_amdgcn_sched_barrier(0);
-        if (wait_dma)
-            __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's copies landed
-        __syncthreads();
+        if (wait_copies)
+            wait_vmcnt(0);
+        barrier_no_fence();
         __builtin_amdgcn_sched_barrier(0);
+    };
+    // Copies of K(j+1) and V(j) into stage (j+1) & 1 (clamped sources: copies
+    // for steps past the last one land in parts of the stage nobody reads).
+    auto plan_step_copies = [&](int j) {
+        cp_k = plan_copy(kbase, step_key0(min(j + 1, nsteps - 1)), (j + 1) & 1, false);
+        cp_v = plan_copy(vbase, step_key0(min(j, nsteps - 1)), (j + 1) & 1, true);
     };
 
     if (nsteps > 0) {
-        dma_step(step_key0(0), 0, true, false);
+        // Prologue: the copy waves copy K(0) into stage 0.
+        if (copy_wave) {
+            cp_k = plan_copy(kbase, step_key0(0), 0, false);
+#pragma unroll
+            for (int c = 0; c < COPIES; ++c)
+                issue_slot(c);
+        }
         end_phase(true);
         if (group == 0) {
-            for (int j = 0; j <= nsteps; ++j) {
-                fetch(j);
-                do_m(j);
+            // j = 0: QK only, then the copies of the PV slots.
+            plan_step_copies(0);
+            do_m(0, true, false, copy_hook);
+#pragma unroll
+            for (int c = 0; c < 2 * COPIES; ++c)
+                if (c * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
+                    issue_slot(c);
+            end_phase(false);
+            do_x(0);
+            end_phase(true);
+            for (int j = 1; j < nsteps; ++j) {
+                plan_step_copies(j);
+                do_m(j, true, true, copy_hook);
                 end_phase(false);
-                if (j < nsteps)
-                    do_x(j);
+                do_x(j);
                 end_phase(true);
             }
+            do_m(nsteps, false, true, no_hook);
+            end_phase(false);
+            end_phase(false);
         } else {
-            for (int j = 0; j <= nsteps; ++j) {
-                fetch(j);
-                if (j >= 1)
-                    do_x(j - 1);
+            end_phase(false);
+            do_m(0, true, false, no_hook);
+            end_phase(false);
+            for (int j = 1; j < nsteps; ++j) {
+                do_x(j - 1);
                 end_phase(false);
-                do_m(j);
-                end_phase(true);
+                do_m(j, true, true, no_hook);
+                end_phase(false);
             }
+            do_x(nsteps - 1);
+            end_phase(false);
+            do_m(nsteps, false, true, no_hook);
+            end_phase(false);
         }
     }
 
