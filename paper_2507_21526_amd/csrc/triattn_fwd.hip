@@ -308,27 +308,33 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const bool copy_wave = wave < N_COPY_WAVES;
     const int dma_row_in = lane / CHUNKS;
     const int dma_pc = lane % CHUNKS;
+    // The swizzle of row m * ROWS_PER_DMA + i is swizzle(i) ^ swizzle of the
+    // copy's first row (K) or swizzle(i) (V), so two per-lane constants give
+    // the stored chunk of every copy.
+    const uint32_t kx0 = (uint32_t)((dma_pc ^ kswz<D>(dma_row_in)) << 4);
+    const uint32_t vx0 = (uint32_t)((dma_pc ^ vswz<D>(dma_row_in)) << 4);
+    const uint32_t row_stride_bytes = 2u * (uint32_t)tok_stride;  // < 2^24 (host check)
     // Keys past the end of the sequence are read from its last row: they lie
     // beyond every row of the item, so the causal mask gives them p = 0.
     const int key_max = seq_len - 1;
     const uint32_t smem_addr =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
 
-    // One tile copy (K or V of one step into one stage).  The lane offset of
-    // a copy is an unsigned 32-bit byte offset from a scalar base at key
-    // min(first key, last key of the sequence): row r of the tile reads key
-    // min(key0 + r, last key), so every offset is non-negative and below 64
-    // rows, and a step past the end of the sequence still reads valid rows.
+    // One tile copy (K or V of one step into one stage).  Row r of the tile
+    // reads key min(key0 + r, last key of the sequence), so a step past the
+    // end of the sequence still reads valid rows.  Copy m starts from the
+    // scalar base key b = min(key0 + m * ROWS_PER_DMA, last key) and lane
+    // row i adds min(i, last key - b) rows: an unsigned 32-bit byte offset
+    // that is never negative.
     struct TileCopy {
-        const uint16_t *base;
+        const uint16_t *src;
         uint32_t lds;
-        int key0, key_base;
+        int key0;
     };
     auto plan_copy = [&](const uint16_t *src, int key0, int buf, bool is_v) -> TileCopy {
         TileCopy t;
+        t.src = src;
         t.key0 = key0;
-        t.key_base = min(key0, key_max);
-        t.base = src + (int64_t)t.key_base * tok_stride;
         t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0);
         return t;
     };
@@ -339,10 +345,13 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
             if (m >= N_DMA)
                 return;
         }
-        const int r = m * ROWS_PER_DMA + dma_row_in;
-        const int kr = min(t.key0 + r, key_max) - t.key_base;  // in [0, 64)
-        const int off = kr * tok_stride + (dma_pc ^ (is_v ? vswz<D>(r) : kswz<D>(r))) * 8;
-        copy_to_lds16(t.base, 2u * (uint32_t)off, t.lds + m * 1024);
+        const int sc = m * ROWS_PER_DMA;
+        const int base_key = min(t.key0 + sc, key_max);
+        const int lim = key_max - base_key;
+        const uint16_t *base = t.src + (int64_t)base_key * tok_stride;
+        const uint32_t xr = is_v ? vx0 : (kx0 ^ (uint32_t)(kswz<D>(sc) << 4));
+        const uint32_t off = __umul24((uint32_t)min(dma_row_in, lim), row_stride_bytes) + xr;
+        copy_to_lds16(base, off, t.lds + m * 1024);
     };
     // Copy slot c (0 <= c < 2 * COPIES): K copies first, then V copies.
     TileCopy cp_k{}, cp_v{};
@@ -361,18 +370,22 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
 
     // S^T = K Q^T for one 64-key step from LDS stage `buf`; the two 32-key
     // accumulator chains alternate so that dependent MFMAs do not stall.
-    const int krow0 = perm_row(col), krow1 = 32 + perm_row(col);
+    // K fragment (kb, s): row kb * 32 + perm_row(col), chunk (2s + half) ^
+    // kswz(row); the swizzle does not depend on kb, so one offset per s.
+    const int krow0 = perm_row(col);
+    uint32_t koff[QK_STEPS];
+#pragma unroll
+    for (int s = 0; s < QK_STEPS; ++s)
+        koff[s] = (uint32_t)(krow0 * ROW_BYTES + (((2 * s + half) ^ kswz<D>(krow0)) << 4));
     auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) {
         const unsigned char *kt = smem + buf * STAGE_BYTES;
         sacc[0] = f32x16{};
         sacc[1] = f32x16{};
 #pragma unroll
         for (int s = 0; s < QK_STEPS; ++s) {
-            const int ch = 2 * s + half;
-            const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(
-                kt + krow0 * ROW_BYTES + ((ch ^ kswz<D>(krow0)) << 4));
-            const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(
-                kt + krow1 * ROW_BYTES + ((ch ^ kswz<D>(krow1)) << 4));
+            const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(kt + koff[s]);
+            const bf16x8 a1 =
+                *reinterpret_cast<const bf16x8 *>(kt + koff[s] + 32 * ROW_BYTES);
             sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], sacc[0], 0, 0, 0);
             hook(2 * s);
             sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], sacc[1], 0, 0, 0);
@@ -398,8 +411,18 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     // fragment of 8 keys x 1 d comes from two transposed reads: in each group
     // of 16 lanes, lane i addresses row K0 + i/4 at d = D0 + 4 (i % 4), and
     // lane j receives rows K0..K0+3 at d = D0 + j.
-    const int tr_row = (lane & 15) >> 2;                       // + K0
+    // Rows differ from 8 half + i/4 by multiples of 4, which leave the V
+    // swizzle unchanged, so one offset per d block plus an immediate covers
+    // every read.
+    const int vrow0 = 8 * half + ((lane & 15) >> 2);
     const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);  // + 32 b
+    uint32_t voff[D_BLOCKS];
+#pragma unroll
+    for (int b = 0; b < D_BLOCKS; ++b) {
+        const int d = 32 * b + tr_d;
+        voff[b] = (uint32_t)(vrow0 * ROW_BYTES + (((d >> 3) ^ vswz<D>(vrow0)) << 4) +
+                             (d & 7) * 2);
+    }
     auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) {
         const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
 #pragma unroll
@@ -410,14 +433,10 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
                 for (int b = 0; b < D_BLOCKS; ++b) {
                     s16x4 part[2];
 #pragma unroll
-                    for (int i2 = 0; i2 < 2; ++i2) {
-                        const int r = kb * 32 + s2 * 16 + 8 * half + 4 * i2 + tr_row;
-                        const int d = 32 * b + tr_d;
-                        const int off = r * ROW_BYTES + (((d >> 3) ^ vswz<D>(r)) << 4) +
-                                        (d & 7) * 2;
+                    for (int i2 = 0; i2 < 2; ++i2)
                         part[i2] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                            (lds_s16x4 *)(vt + off));
-                    }
+                            (lds_s16x4 *)(vt + voff[b] +
+                                          (kb * 32 + s2 * 16 + 4 * i2) * ROW_BYTES));
                     const bf16x8 af = __builtin_bit_cast(
                         bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5,
                                                         6, 7));
@@ -831,6 +850,9 @@ ta_status check_common(const char *fn, int want_kind, const void *q, const void 
     const int64_t subtiles = info->tile / rows_per_wg(hq / hkv, info->tile);
     if ((int64_t)info->n_items * subtiles * hkv > INT32_MAX)
         return fail(TA_ERR_UNSUPPORTED, "%s: grid too large", fn);
+    // per-lane copy offsets use 24-bit multiplies of the key row pitch
+    if (2LL * hkv * head_dim >= (1LL << 24))
+        return fail(TA_ERR_UNSUPPORTED, "%s: hkv * head_dim too large", fn);
     return TA_OK;
 }
 
