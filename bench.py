@@ -99,7 +99,7 @@ def summarize(root, workload):
     os.makedirs(prof, exist_ok=True)
     cmd = "rocprofv3 --kernel-trace --stats --output-format csv -d <dir>/trace " \
           f"-- python3 bench.py --workload {workload} --steps 5 --warmup 1 " \
-          "--no-cpu-baseline"
+          "--no-cpu-baseline --no-extra"
     stats = glob.glob(os.path.join(root, "trace", "**", "*kernel_stats.csv"),
                       recursive=True)
     if stats:
@@ -171,10 +171,10 @@ def summarize(root, workload):
             "commands": [
                 "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir>/fetch "
                 f"-- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
-                "--no-dense --no-cpu-baseline --copy-calibration",
+                "--no-dense --no-cpu-baseline --no-extra --copy-calibration",
                 "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir>/write "
                 f"-- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
-                "--no-dense --no-cpu-baseline --copy-calibration",
+                "--no-dense --no-cpu-baseline --no-extra --copy-calibration",
             ],
         }
         with open(os.path.join(prof, f"traffic_tile_kernel_{workload}.json"), "w") as out:
@@ -259,6 +259,120 @@ def time_loop(fn_steps, steps, warmup, torch):
     return wall, events
 
 
+def gpu_qkv(total, hq, hkv, d, seed, dev, torch):
+    """Seeded N(0, 1) bf16 Q/K/V drawn on the device (timing sections only:
+    the run time does not depend on the values, and drawing 128K-token
+    layers on the host would dominate the run)."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    out = []
+    for h in (hq, hkv, hkv):
+        out.append(torch.randn((total, h, d), device=dev, generator=g,
+                               dtype=torch.float32).to(torch.bfloat16))
+    return out
+
+
+def timed_pass(binding, plan, q, k, v, o, scale, stream, steps, warmup, torch):
+    """Mean kernel time (ms, HIP events on the launch stream) of one full
+    pass: Triangle tiles + merge, or dense causal."""
+    def run():
+        if plan.kind == binding.TRIANGLE:
+            binding.triangle_attn_fwd(q, k, v, o, None, plan.sched, plan.info, scale,
+                                      plan.workspace, stream)
+        else:
+            binding.causal_attn_fwd(q, k, v, o, None, plan.sched, plan.info, scale,
+                                    stream)
+    for _ in range(warmup):
+        run()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def kept_flops(info, hq, tile, d):
+    return float(info.kept_tiles_per_qhead) * hq * 4.0 * tile * tile * d
+
+
+def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch):
+    """Timing of the other workloads: the varlen batch (per-sequence
+    schedules), the 28-layer Qwen stack (mixed vs all-dense), and the 128K
+    Llama layer at the paper's own Streaming shape (S = 8, W = 512)."""
+    stream = torch.cuda.current_stream()
+    out = {}
+
+    # variable-length packed batch
+    w = WORKLOADS["llama8b_varlen4"]
+    cu = list(w.cu_seqlens)
+    q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+    o = torch.empty_like(q)
+    tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                       device=dev)
+    den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                       device=dev)
+    t_tri = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 10, 2, torch)
+    t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 2, 1, torch)
+    out["varlen"] = {
+        "workload": w.name, "cu_seqlens": cu,
+        "triangle_ms": t_tri, "dense_ms": t_den,
+        "triangle_kept_tile_tflops": kept_flops(tri.info, w.hq, w.tile, w.d) / t_tri / 1e9,
+        "dense_kept_tile_tflops": kept_flops(den.info, w.hq, w.tile, w.d) / t_den / 1e9,
+        "speedup_vs_dense": t_den / t_tri,
+        "ideal_kept_tile_ratio": den.info.kept_tiles_per_qhead / tri.info.kept_tiles_per_qhead,
+    }
+    del q, k, v, o, tri, den
+
+    # 28-layer Qwen stack: 20 Triangle layers (seeded choice) and 8 dense
+    w = WORKLOADS["qwen7b_n128k_stack28"]
+    cu = list(w.cu_seqlens)
+    tri_layers = set(triangle_layer_set(w))
+    tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                       device=dev)
+    den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                       device=dev)
+    mixed = all_dense = 0.0
+    per_layer = []
+    for layer in range(w.layers):
+        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed * 1000 + layer, dev, torch)
+        o = torch.empty_like(q)
+        t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 1, 1, torch)
+        t_use = t_den
+        if layer in tri_layers:
+            t_use = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 3, 1, torch)
+        mixed += t_use
+        all_dense += t_den
+        per_layer.append(round(t_use, 3))
+        del q, k, v, o
+    out["stack"] = {
+        "workload": w.name, "layers": w.layers,
+        "triangle_layers": sorted(tri_layers),
+        "mixed_ms": mixed, "all_dense_ms": all_dense,
+        "speedup_vs_all_dense": all_dense / mixed,
+        "per_layer_ms": per_layer,
+    }
+
+    # the paper's Streaming shape on the 128K Llama layer
+    w = WORKLOADS["llama8b_n128k"]
+    cu = list(w.cu_seqlens)
+    q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+    o = torch.empty_like(q)
+    ps = binding.Plan("triangle", cu, 8, 512, w.last, w.tile, w.hq, w.d, device=dev)
+    t_ps = timed_pass(binding, ps, q, k, v, o, w.scale, stream, 10, 2, torch)
+    out["paper_shape"] = {
+        "workload": w.name, "sink": 8, "window": 512, "last": w.last, "tile": w.tile,
+        "triangle_ms": t_ps,
+        "kept_tile_tflops": kept_flops(ps.info, w.hq, w.tile, w.d) / t_ps / 1e9,
+        "speedup_vs_dense": (dense_128k_ms / t_ps) if dense_128k_ms else None,
+        "note": "paper's 15.3x at 128K (A100, Triton vs FlashAttention) used sink 8, "
+                "window 512; its number of Last rows is not stated, 128 here",
+    }
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -268,6 +382,8 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the varlen, 28-layer stack and paper-shape timings")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy first (reference "
@@ -292,7 +408,7 @@ def main():
     import torch
 
     from paper_2507_21526_amd import binding
-    from paper_2507_21526_amd.inputs import WORKLOADS, workload_qkv
+    from paper_2507_21526_amd.inputs import WORKLOADS, triangle_layer_set, workload_qkv
 
     w = WORKLOADS[args.workload]
     assert w.layers == 1, "the benchmark times one attention layer"
@@ -376,6 +492,12 @@ def main():
         log(f"timing the fp64 oracle on a row sample (~{args.cpu_seconds:.0f} s)")
         cpu = cpu_baseline(w, q, k, v, args.cpu_seconds, kept_flops)
 
+    extra = None
+    if not args.no_extra:
+        log("timing the varlen batch, the 28-layer stack and the paper shape")
+        extra = extra_sections(binding, WORKLOADS, triangle_layer_set,
+                               dense_rec["ms_per_step"] if dense_rec else None, dev, torch)
+
     traffic = load_traffic(w.name)
     rec = {
         "metric": "Triangle-attn prefill TFLOP/s (kept tiles) + speedup vs dense causal @128K",
@@ -415,6 +537,7 @@ def main():
                   (merge_gbs / PEAK_HBM_GBS) if merge_gbs else None},
         "dense_causal": dense_rec,
         "speedup_vs_dense": (dense_rec["ms_per_step"] / ms_per_step) if dense_rec else None,
+        "other_workloads": extra,
         "schedule": {"build_us_host": sched_build_us, "items": info.n_items,
                      "kept_tiles_per_qhead": info.kept_tiles_per_qhead,
                      "last_splits": info.max_splits},

@@ -743,17 +743,45 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 #pragma unroll
     for (int e = 0; e < PER; ++e)
         acc[e] = 0.f;
-    for (int c = 0; c < ns; ++c) {
-        const float wgt = __expf(lse_of(c) - m_use);
-        const float *po =
-            a.part_o + (((int64_t)pb + (int64_t)c * rows + rank) * a.hq + head) * D;
+    // Partial rows of consecutive splits lie rows * hq * D floats apart; the
+    // loads of UNROLL splits are issued before any is used, so the wave keeps
+    // that many rows in flight (the sum still runs in split order).
+    const int64_t split_stride = (int64_t)rows * a.hq * D;
+    const float *po0 = a.part_o + (((int64_t)pb + rank) * a.hq + head) * D + PER * lane;
+    auto load_row = [&](int c, float (&t)[PER]) {
+        const float *po = po0 + (int64_t)c * split_stride;
         if constexpr (PER == 2) {
-            const f32x2 t = *reinterpret_cast<const f32x2 *>(po + 2 * lane);
-            acc[0] += wgt * t[0];
-            acc[PER - 1] += wgt * t[1];
+            const f32x2 v = *reinterpret_cast<const f32x2 *>(po);
+            t[0] = v[0];
+            t[PER - 1] = v[1];
         } else {
-            acc[0] += wgt * po[lane];
+            t[0] = po[0];
         }
+    };
+    constexpr int UNROLL = 8;
+    int c = 0;
+    for (; c + UNROLL <= ns; c += UNROLL) {
+        float t[UNROLL][PER], l[UNROLL];
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            load_row(c + u, t[u]);
+            l[u] = lse_of(c + u);
+        }
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            const float wgt = __expf(l[u] - m_use);
+#pragma unroll
+            for (int e = 0; e < PER; ++e)
+                acc[e] += wgt * t[u][e];
+        }
+    }
+    for (; c < ns; ++c) {
+        float t[PER];
+        load_row(c, t);
+        const float wgt = __expf(lse_of(c) - m_use);
+#pragma unroll
+        for (int e = 0; e < PER; ++e)
+            acc[e] += wgt * t[e];
     }
     const float inv = den > 0.f ? 1.f / den : 0.f;
     const int64_t orow = ((seq_off + row) * a.hq + head) * (int64_t)D;
