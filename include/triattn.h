@@ -66,7 +66,11 @@ typedef enum {
     TA_ERR_HIP = 6               /* a HIP launch call failed */
 } ta_status;
 
-typedef enum { TA_KIND_TRIANGLE = 0, TA_KIND_CAUSAL = 1 } ta_kind;
+typedef enum {
+    TA_KIND_TRIANGLE = 0,   /* Triangle attention (ta_build_schedule) */
+    TA_KIND_CAUSAL = 1,     /* dense causal attention (ta_build_schedule) */
+    TA_KIND_BLOCKSPARSE = 2 /* caller-listed k-tiles (ta_build_blocksparse_schedule) */
+} ta_kind;
 typedef enum { TA_OUT_BF16 = 0, TA_OUT_F32 = 1 } ta_out_dtype;
 
 /* Summary of a built schedule (mirrors the header words of the packed form). */
@@ -79,12 +83,13 @@ typedef struct ta_schedule_info {
     int32_t splits_requested; /* 0 = automatic split rule */
     int64_t total_tokens;
     int64_t words;            /* int32 words of the packed schedule */
-    int32_t n_items;          /* main-pass work items (Last splits first) */
-    int32_t n_last_items;     /* of which Last-row split items */
-    int32_t n_merge_items;    /* Last q-tiles (one merge each) */
+    int32_t n_items;          /* main-pass work items (split items first) */
+    int32_t n_last_items;     /* of which split items (Last rows or split
+                                 block-sparse q-tiles) */
+    int32_t n_merge_items;    /* split q-tiles (one merge each) */
     int32_t n_last_rows;      /* rows covered by merge items */
     int32_t n_partial_rows;   /* rows of split partials in the workspace */
-    int32_t max_splits;       /* largest split count of a Last q-tile */
+    int32_t max_splits;       /* largest split count of a q-tile */
     int64_t kept_tiles_per_qhead; /* kept (q-tile, k-tile) pairs per head */
 } ta_schedule_info;
 
@@ -118,8 +123,51 @@ ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
                             int32_t *out, int64_t out_words,
                             ta_schedule_info *info);
 
-/* Bytes of workspace triangle_attn_fwd needs for the split partials of the
- * Last rows (fp32 partial outputs and their LSE); 0 when there are none. */
+/*
+ * Build the schedule of block-sparse causal attention on the host: the same
+ * tile passes driven by a caller-supplied list of kept k-tiles per q-tile.
+ * This is the attention of the layers TriangleMix keeps dense when they are
+ * handed to a dynamic sparse method instead (Sec. 2.4; the "Ours + X"
+ * combinations of Sec. 3.1), whose index estimator produces such lists.
+ *   Row i (0-indexed in its sequence, q-tile i / tile) keeps key j iff
+ *   j <= i and k-tile j / tile is listed for that q-tile.  A row that keeps
+ *   no key gets a zero output row and lse = -inf.
+ *   cu_seqlens  as for ta_build_schedule.
+ *   tile        64 or 128.
+ *   qtile_ptr   host array of Q + 1 int32, Q = sum over sequences of
+ *               ceil(n_b / tile) (q-tiles in sequence order): the k-tiles of
+ *               global q-tile t are ktile_idx[qtile_ptr[t] .. qtile_ptr[t+1]).
+ *               qtile_ptr[0] = 0, non-decreasing.
+ *   ktile_idx   host array of sequence-relative k-tile indices, strictly
+ *               increasing per q-tile, each in [0, q-tile index] (tiles
+ *               above the diagonal hold no key j <= i and are rejected).
+ *               May be NULL when every list is empty.
+ *   max_tiles_per_item  work bound per item (0 = 16): each q-tile's listed
+ *               k-tiles form maximal runs of consecutive tiles; runs longer
+ *               than the bound are cut into consecutive pieces of at most
+ *               the bound; pieces are packed in order into items of at most
+ *               two pieces and at most the bound in tiles (a piece joins the
+ *               current item when it holds one piece and the sum fits).  A
+ *               q-tile with one item writes its rows directly; one with
+ *               several gets split items (normalised fp32 partials in the
+ *               workspace) and a merge item, as the Last rows of Triangle
+ *               attention.  Items are ordered split items first, each group
+ *               by decreasing tile count (stable); merge items in q-tile
+ *               order.  A q-tile with an empty list gets one item of no
+ *               tile.
+ *   out, out_words, info  as for ta_build_schedule; info->kind is
+ *               TA_KIND_BLOCKSPARSE, sink = window = last = 0 and
+ *               splits_requested = max_tiles_per_item.
+ */
+ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens, int32_t batch,
+                                        int32_t tile, const int32_t *qtile_ptr,
+                                        const int32_t *ktile_idx,
+                                        int32_t max_tiles_per_item, int32_t *out,
+                                        int64_t out_words, ta_schedule_info *info);
+
+/* Bytes of workspace triangle_attn_fwd (or blocksparse_attn_fwd) needs for
+ * the split partials (fp32 partial outputs and their LSE); 0 when there are
+ * none. */
 size_t ta_workspace_bytes(const ta_schedule_info *info, int32_t hq,
                           int32_t head_dim);
 
@@ -186,6 +234,21 @@ ta_status causal_attn_fwd(const void *q, const void *k, const void *v,
                           const ta_schedule_info *info, int64_t total_tokens,
                           int32_t hq, int32_t hkv, int32_t head_dim,
                           float softmax_scale, void *stream);
+
+/*
+ * Block-sparse causal attention forward over a TA_KIND_BLOCKSPARSE schedule
+ * (Sec. 2.4 and 3.1, "Ours + X": the dense layers replaced by a dynamic
+ * sparse method): the tile pass over every item, then the LSE-weighted merge
+ * of the split q-tiles.  Same arguments and workspace rule as
+ * triangle_attn_fwd.
+ */
+ta_status blocksparse_attn_fwd(const void *q, const void *k, const void *v,
+                               void *o, int32_t o_dtype, float *lse,
+                               const int32_t *sched_dev,
+                               const ta_schedule_info *info, int64_t total_tokens,
+                               int32_t hq, int32_t hkv, int32_t head_dim,
+                               float softmax_scale, void *workspace,
+                               size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -10,7 +10,10 @@ baseline leg of the benchmark may import this package; the product path
 * attention: the masked softmax of Sec. 2.1, row by row, masked logits
   removed exactly;
 * tile schedule: brute force over every (q-tile, k-tile) block, emitted in
-  the documented packed int32 format.
+  the documented packed int32 format;
+* block-sparse causal attention (the dense layers handed to a dynamic sparse
+  method, Sec. 2.4 and Sec. 3.1): a row keeps key j iff j <= i and the
+  k-tile of j is listed for the row's q-tile.
 
 This module only marshals arguments through ctypes and compiles the C file
 with gcc when no built library is present.
@@ -68,6 +71,13 @@ def load():
     lib.oracle_schedule.argtypes = [ctypes.c_int, vp, i32, i32, i32, i32, i32,
                                     i32, vp, i64]
     lib.oracle_schedule.restype = i64
+    lib.oracle_bs_mask.argtypes = [i64, i64, i64, vp, i64]
+    lib.oracle_bs_mask.restype = ctypes.c_int
+    lib.oracle_attn_rows_bs.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32,
+                                        vp, vp, dbl, vp, vp, i64, vp, vp]
+    lib.oracle_attn_rows_bs.restype = ctypes.c_int
+    lib.oracle_bs_schedule.argtypes = [vp, i32, i32, vp, vp, i32, vp, i64]
+    lib.oracle_bs_schedule.restype = i64
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -172,5 +182,73 @@ def schedule(kind, cu_seqlens, sink, window, last, tile, splits=0) -> np.ndarray
     out = np.zeros(words, dtype=np.int32)
     got = lib.oracle_schedule(_kind(kind), cu.ctypes.data, cu.size - 1, sink,
                               window, last, tile, splits, out.ctypes.data, words)
+    assert got == words
+    return out
+
+
+# ---- block-sparse causal attention ----------------------------------------
+
+def _csr(qtile_ptr, ktile_idx):
+    ptr = np.ascontiguousarray(np.asarray(qtile_ptr, dtype=np.int32))
+    idx = np.ascontiguousarray(np.asarray(ktile_idx, dtype=np.int32))
+    if idx.size == 0:
+        idx = np.zeros(1, dtype=np.int32)  # valid pointer, never read
+    return ptr, idx
+
+
+def bs_mask_row(i, n, tile, kept_tiles) -> np.ndarray:
+    """Mask row i (sequence-relative) given the k-tile list of its q-tile."""
+    lst = np.ascontiguousarray(np.asarray(kept_tiles, dtype=np.int32))
+    if lst.size == 0:
+        lst = np.zeros(1, dtype=np.int32)
+        ln = 0
+    else:
+        ln = lst.size
+    lib = load()
+    return np.array([lib.oracle_bs_mask(i, j, tile, lst.ctypes.data, ln)
+                     for j in range(n)], dtype=np.uint8)
+
+
+def bs_mask_matrix(n, tile, lists) -> np.ndarray:
+    """Full n x n block-sparse mask of one sequence; lists[t] = k-tiles of
+    q-tile t (small n only)."""
+    return np.stack([bs_mask_row(i, n, tile, lists[i // tile]) for i in range(n)]) \
+        if n > 0 else np.zeros((0, 0), np.uint8)
+
+
+def attn_rows_bs(q, k, v, cu_seqlens, tile, qtile_ptr, ktile_idx, scale,
+                 row_tok, row_head):
+    """Block-sparse causal attention rows: (out [nrows, d], lse [nrows])."""
+    qb, kb, vb = _bf16_bits(q), _bf16_bits(k), _bf16_bits(v)
+    total, hq, d = qb.shape
+    hkv = kb.shape[1]
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    ptr, idx = _csr(qtile_ptr, ktile_idx)
+    rt = np.ascontiguousarray(np.asarray(row_tok, dtype=np.int64))
+    rh = np.ascontiguousarray(np.asarray(row_head, dtype=np.int32))
+    out = np.zeros((rt.size, d), dtype=np.float64)
+    lse = np.zeros(rt.size, dtype=np.float64)
+    rc = load().oracle_attn_rows_bs(qb.ctypes.data, kb.ctypes.data, vb.ctypes.data,
+                                    cu.ctypes.data, cu.size - 1, hq, hkv, d, tile,
+                                    ptr.ctypes.data, idx.ctypes.data, float(scale),
+                                    rt.ctypes.data, rh.ctypes.data, rt.size,
+                                    out.ctypes.data, lse.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_attn_rows_bs rejected the request")
+    return out, lse
+
+
+def schedule_bs(cu_seqlens, tile, qtile_ptr, ktile_idx, max_tiles=0) -> np.ndarray:
+    """Block-sparse schedule in the packed int32 format."""
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    ptr, idx = _csr(qtile_ptr, ktile_idx)
+    lib = load()
+    words = lib.oracle_bs_schedule(cu.ctypes.data, cu.size - 1, tile, ptr.ctypes.data,
+                                   idx.ctypes.data, max_tiles, None, 0)
+    if words < 0:
+        raise ValueError("oracle_bs_schedule rejected the lists")
+    out = np.zeros(words, dtype=np.int32)
+    got = lib.oracle_bs_schedule(cu.ctypes.data, cu.size - 1, tile, ptr.ctypes.data,
+                                 idx.ctypes.data, max_tiles, out.ctypes.data, words)
     assert got == words
     return out

@@ -93,12 +93,36 @@ int64_t oracle_mask_nnz(int kind, int64_t n, int64_t sink, int64_t window,
 
 /* ---- Sec. 2.1: masked softmax attention, one (row, head) at a time ---- */
 
-int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
-                     const int32_t *cu_seqlens, int32_t batch, int32_t hq,
-                     int32_t hkv, int32_t d, int kind, int64_t sink,
-                     int64_t window, int64_t last, double scale,
-                     const int64_t *row_tok, const int32_t *row_head,
-                     int64_t nrows, double *out, double *lse)
+/* Mask row source: fills row[0..n) for row i of sequence b. */
+typedef struct {
+    int kind;
+    int64_t sink, window, last;
+    /* block-sparse lists (kind < 0) */
+    int64_t tile;
+    const int32_t *qtile_ptr, *ktile_idx, *qbase;
+} mask_src;
+
+static void fill_mask_row(const mask_src *ms, int32_t b, int64_t n, int64_t i,
+                          uint8_t *row)
+{
+    if (ms->kind >= 0) {
+        oracle_mask_row(ms->kind, n, ms->sink, ms->window, ms->last, i, row);
+        return;
+    }
+    const int64_t g = ms->qbase[b] + i / ms->tile;
+    const int32_t *list = ms->ktile_idx + ms->qtile_ptr[g];
+    const int64_t len = ms->qtile_ptr[g + 1] - ms->qtile_ptr[g];
+    for (int64_t j = 0; j < n; ++j)
+        row[j] = (uint8_t)oracle_bs_mask(i, j, ms->tile, list, len);
+}
+
+/* Masked softmax attention of the requested rows (Sec. 2.1). */
+static int attn_rows_core(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                          const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                          int32_t hkv, int32_t d, const mask_src *ms,
+                          double scale, const int64_t *row_tok,
+                          const int32_t *row_head, int64_t nrows, double *out,
+                          double *lse)
 {
     if (batch < 0 || hq <= 0 || hkv <= 0 || d <= 0 || hq % hkv != 0)
         return -1;
@@ -139,7 +163,7 @@ int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                 bad = 1;
                 continue;
             }
-            oracle_mask_row(kind, n, sink, window, last, i, mask);
+            fill_mask_row(ms, b, n, i, mask);
 
             const uint16_t *qi = q + ((size_t)t * hq + h) * d;
             double zmax = -INFINITY;
@@ -167,15 +191,80 @@ int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                 for (int32_t c = 0; c < d; ++c)
                     o[c] += p * widen_bf16(vj[c]);
             }
-            for (int32_t c = 0; c < d; ++c)
-                o[c] /= denom;
+            if (denom > 0.0) {
+                for (int32_t c = 0; c < d; ++c)
+                    o[c] /= denom;
+            }
             if (lse)
-                lse[r] = zmax + log(denom);
+                lse[r] = denom > 0.0 ? zmax + log(denom) : -INFINITY;
         }
         free(mask);
         free(z);
     }
     return bad ? -1 : 0;
+}
+
+int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                     const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                     int32_t hkv, int32_t d, int kind, int64_t sink,
+                     int64_t window, int64_t last, double scale,
+                     const int64_t *row_tok, const int32_t *row_head,
+                     int64_t nrows, double *out, double *lse)
+{
+    if (kind != ORACLE_TRIANGLE && kind != ORACLE_CAUSAL)
+        return -1;
+    mask_src ms = {kind, sink, window, last, 0, NULL, NULL, NULL};
+    return attn_rows_core(q, k, v, cu_seqlens, batch, hq, hkv, d, &ms, scale,
+                          row_tok, row_head, nrows, out, lse);
+}
+
+/* ---- Block-sparse causal attention ---- */
+
+int oracle_bs_mask(int64_t i, int64_t j, int64_t tile, const int32_t *list,
+                   int64_t len)
+{
+    if (j > i)
+        return 0;
+    const int64_t kt = j / tile;
+    for (int64_t p = 0; p < len; ++p)
+        if (list[p] == kt)
+            return 1;
+    return 0;
+}
+
+/* First global q-tile of each sequence; returns NULL on failure. */
+static int32_t *qtile_bases(const int32_t *cu_seqlens, int32_t batch, int64_t tile)
+{
+    int32_t *base = (int32_t *)malloc(sizeof(int32_t) * (size_t)(batch + 1));
+    if (!base)
+        return NULL;
+    int64_t acc = 0;
+    for (int32_t b = 0; b < batch; ++b) {
+        base[b] = (int32_t)acc;
+        acc += (cu_seqlens[b + 1] - cu_seqlens[b] + tile - 1) / tile;
+    }
+    base[batch] = (int32_t)acc;
+    return base;
+}
+
+int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                        const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                        int32_t hkv, int32_t d, int32_t tile,
+                        const int32_t *qtile_ptr, const int32_t *ktile_idx,
+                        double scale, const int64_t *row_tok,
+                        const int32_t *row_head, int64_t nrows, double *out,
+                        double *lse)
+{
+    if (tile < 1 || batch < 0)
+        return -1;
+    int32_t *base = qtile_bases(cu_seqlens, batch, tile);
+    if (!base)
+        return -1;
+    mask_src ms = {-1, 0, 0, 0, tile, qtile_ptr, ktile_idx, base};
+    const int rc = attn_rows_core(q, k, v, cu_seqlens, batch, hq, hkv, d, &ms,
+                                  scale, row_tok, row_head, nrows, out, lse);
+    free(base);
+    return rc;
 }
 
 /* ---- Tile schedule by brute force over blocks ----
@@ -222,6 +311,19 @@ static int push_item(item_vec *iv, const item_t *it)
     }
     iv->v[iv->n++] = *it;
     return 0;
+}
+
+static void stable_sort_by_cost(item_vec *iv)
+{
+    for (int64_t a = 1; a < iv->n; ++a) {
+        item_t x = iv->v[a];
+        int64_t p = a - 1;
+        while (p >= 0 && iv->v[p].w[10] < x.w[10]) {
+            iv->v[p + 1] = iv->v[p];
+            --p;
+        }
+        iv->v[p + 1] = x;
+    }
 }
 
 /* kept[qt * nkt + kt] = 1 iff block (q-tile qt, k-tile kt) holds a kept pair.
@@ -363,19 +465,10 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
         }
     }
 
-    if (!fail && kind == ORACLE_CAUSAL) {
+    if (!fail && kind == ORACLE_CAUSAL)
         /* stable ordering by kept k-tiles, descending (insertion sort keeps
          * equal costs in their (sequence, q-tile) order) */
-        for (int64_t a = 1; a < main_items.n; ++a) {
-            item_t x = main_items.v[a];
-            int64_t p = a - 1;
-            while (p >= 0 && main_items.v[p].w[10] < x.w[10]) {
-                main_items.v[p + 1] = main_items.v[p];
-                --p;
-            }
-            main_items.v[p + 1] = x;
-        }
-    }
+        stable_sort_by_cost(&main_items);
 
     int64_t words = -1;
     if (!fail) {
@@ -411,6 +504,148 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
     }
     free(last_items.v);
     free(main_items.v);
+    free(merges.v);
+    return words;
+}
+
+int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
+                           int32_t tile, const int32_t *qtile_ptr,
+                           const int32_t *ktile_idx, int32_t max_tiles,
+                           int32_t *out, int64_t cap)
+{
+    if (batch < 0 || tile < 1 || max_tiles < 0 || cu_seqlens[0] != 0 ||
+        qtile_ptr[0] != 0)
+        return -1;
+    for (int32_t b = 0; b < batch; ++b)
+        if (cu_seqlens[b + 1] < cu_seqlens[b])
+            return -1;
+    const int64_t bound = max_tiles > 0 ? max_tiles : 16;
+    item_vec split_items = {0}, items = {0}, merges = {0};
+    int64_t partial_rows = 0, kept_total = 0, merged_rows = 0;
+    int fail = 0;
+    int64_t g = 0; /* global q-tile */
+
+    for (int32_t b = 0; b < batch && !fail; ++b) {
+        const int64_t off = cu_seqlens[b];
+        const int64_t n = cu_seqlens[b + 1] - off;
+        const int64_t nkt = (n + tile - 1) / tile;
+        for (int64_t qt = 0; qt * tile < n && !fail; ++qt, ++g) {
+            const int32_t *list = ktile_idx + qtile_ptr[g];
+            const int64_t len = qtile_ptr[g + 1] - qtile_ptr[g];
+            if (len < 0) {
+                fail = 1;
+                break;
+            }
+            for (int64_t p = 0; p < len; ++p)
+                if (list[p] < 0 || list[p] > qt || (p > 0 && list[p] <= list[p - 1]))
+                    fail = 1;
+            if (fail)
+                break;
+            const int64_t r0 = qt * tile;
+            const int64_t r1 = (r0 + tile < n) ? r0 + tile : n;
+            /* kept k-tiles by brute force over the element mask */
+            uint8_t *kept = (uint8_t *)calloc((size_t)(nkt > 0 ? nkt : 1), 1);
+            if (!kept) {
+                fail = 1;
+                break;
+            }
+            for (int64_t kt = 0; kt < nkt; ++kt) {
+                const int64_t c0 = kt * tile;
+                const int64_t c1 = (c0 + tile < n) ? c0 + tile : n;
+                int any = 0;
+                for (int64_t i = r0; i < r1 && !any; ++i)
+                    for (int64_t j = c0; j < c1 && !any; ++j)
+                        any = oracle_bs_mask(i, j, tile, list, len);
+                kept[kt] = (uint8_t)any;
+            }
+            /* pieces: runs of kept k-tiles cut at the bound; items: up to two
+             * pieces and the bound in tiles */
+            item_vec q_items = {0};
+            int pieces_in_last = 0;
+            for (int64_t kt = 0; kt < nkt && !fail;) {
+                if (!kept[kt]) {
+                    ++kt;
+                    continue;
+                }
+                int64_t e = kt;
+                while (e < nkt && kept[e])
+                    ++e;
+                for (int64_t a = kt; a < e && !fail; a += bound) {
+                    const int64_t z = (a + bound < e) ? a + bound : e;
+                    item_t *cur = q_items.n ? &q_items.v[q_items.n - 1] : NULL;
+                    if (cur && pieces_in_last == 1 && cur->w[10] + (z - a) <= bound) {
+                        cur->w[6] = (int32_t)a;
+                        cur->w[7] = (int32_t)z;
+                        cur->w[10] += (int32_t)(z - a);
+                        pieces_in_last = 2;
+                    } else {
+                        item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
+                                      (int32_t)a, (int32_t)z, 0, 0, 1, -1,
+                                      (int32_t)(z - a), 0}};
+                        fail |= push_item(&q_items, &it);
+                        pieces_in_last = 1;
+                    }
+                }
+                kt = e;
+            }
+            free(kept);
+            kept_total += len;
+            if (!fail && q_items.n == 0) {
+                item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1, 0, 0,
+                              0, 0, 1, -1, 0, 0}};
+                fail |= push_item(&q_items, &it);
+            }
+            if (!fail && q_items.n == 1) {
+                fail |= push_item(&items, &q_items.v[0]);
+            } else if (!fail) {
+                const int64_t ns = q_items.n;
+                for (int64_t c = 0; c < ns; ++c) {
+                    q_items.v[c].w[9] = (int32_t)(partial_rows + c * (r1 - r0));
+                    fail |= push_item(&split_items, &q_items.v[c]);
+                }
+                item_t m = {{(int32_t)off, (int32_t)r0, (int32_t)r1, (int32_t)ns,
+                             (int32_t)partial_rows, 0, 0, 0, 0, 0, 0, 0}};
+                fail |= push_item(&merges, &m);
+                partial_rows += ns * (r1 - r0);
+                merged_rows += r1 - r0;
+            }
+            free(q_items.v);
+        }
+    }
+    int64_t words = -1;
+    if (!fail) {
+        stable_sort_by_cost(&split_items);
+        stable_sort_by_cost(&items);
+        const int64_t n_main = split_items.n + items.n;
+        words = HDR_WORDS + n_main * ITEM_WORDS + merges.n * MERGE_WORDS;
+        if (out && cap >= words) {
+            const int64_t total = cu_seqlens[batch];
+            int32_t *w = out;
+            w[0] = SCHED_MAGIC;
+            w[1] = SCHED_VERSION;
+            w[2] = 2; /* block-sparse */
+            w[3] = tile;
+            w[4] = batch;
+            w[5] = w[6] = w[7] = 0;
+            w[8] = max_tiles;
+            w[9] = (int32_t)(uint32_t)((uint64_t)total & 0xffffffffu);
+            w[10] = (int32_t)(uint32_t)((uint64_t)total >> 32);
+            w[11] = (int32_t)n_main;
+            w[12] = (int32_t)merges.n;
+            w[13] = (int32_t)partial_rows;
+            w[14] = (int32_t)kept_total;
+            w[15] = (int32_t)merged_rows;
+            w += HDR_WORDS;
+            for (int64_t a = 0; a < split_items.n; ++a, w += ITEM_WORDS)
+                memcpy(w, split_items.v[a].w, sizeof(int32_t) * ITEM_WORDS);
+            for (int64_t a = 0; a < items.n; ++a, w += ITEM_WORDS)
+                memcpy(w, items.v[a].w, sizeof(int32_t) * ITEM_WORDS);
+            for (int64_t a = 0; a < merges.n; ++a, w += MERGE_WORDS)
+                memcpy(w, merges.v[a].w, sizeof(int32_t) * MERGE_WORDS);
+        }
+    }
+    free(split_items.v);
+    free(items.v);
     free(merges.v);
     return words;
 }

@@ -78,6 +78,37 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
                         int32_t tile, int32_t splits, int32_t *out,
                         int64_t cap);
 
+/*
+ * Block-sparse causal attention (Sec. 2.4 / Sec. 3.1: the dense layers handed
+ * to a dynamic sparse method, whose estimator lists the kept k-tiles of each
+ * q-tile).  Lists are CSR over the q-tiles of all sequences in order
+ * (q-tile t of sequence b has global index sum_{b' < b} ceil(n_b' / tile) + t):
+ * the k-tiles of global q-tile g are ktile_idx[qtile_ptr[g] .. qtile_ptr[g+1]).
+ * Row i keeps key j iff j <= i and floor(j / tile) is listed for q-tile
+ * floor(i / tile).  A row with no kept key has output 0 and lse -inf.
+ */
+int oracle_bs_mask(int64_t i, int64_t j, int64_t tile, const int32_t *list,
+                   int64_t len);
+int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                        const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                        int32_t hkv, int32_t d, int32_t tile,
+                        const int32_t *qtile_ptr, const int32_t *ktile_idx,
+                        double scale, const int64_t *row_tok,
+                        const int32_t *row_head, int64_t nrows, double *out,
+                        double *lse);
+/*
+ * Block-sparse schedule in the packed format: kept blocks by brute force over
+ * oracle_bs_mask, runs of consecutive kept k-tiles cut into pieces of at most
+ * max_tiles (0 = 16), pieces packed in order into items of at most two pieces
+ * and max_tiles tiles; q-tiles with several items get split items and a merge
+ * item; split items first, then the rest, each stable by decreasing tiles.
+ * Returns the number of words, or -1 on invalid lists.
+ */
+int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
+                           int32_t tile, const int32_t *qtile_ptr,
+                           const int32_t *ktile_idx, int32_t max_tiles,
+                           int32_t *out, int64_t cap);
+
 int oracle_num_threads(void);
 
 #ifdef __cplusplus

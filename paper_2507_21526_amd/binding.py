@@ -26,6 +26,7 @@ TA_ERR_HIP = 6
 
 TRIANGLE = 0
 CAUSAL = 1
+BLOCKSPARSE = 2
 OUT_BF16 = 0
 OUT_F32 = 1
 
@@ -99,6 +100,11 @@ def lib():
     L.causal_attn_fwd.restype = ctypes.c_int
     L.causal_attn_fwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, pinfo, i64,
                                   i32, i32, i32, ctypes.c_float, vp]
+    L.ta_build_blocksparse_schedule.restype = ctypes.c_int
+    L.ta_build_blocksparse_schedule.argtypes = [vp, i32, i32, vp, vp, i32, vp, i64,
+                                                pinfo]
+    L.blocksparse_attn_fwd.restype = ctypes.c_int
+    L.blocksparse_attn_fwd.argtypes = list(L.triangle_attn_fwd.argtypes)
     _lib = L
     return L
 
@@ -121,6 +127,8 @@ def _kind(kind) -> int:
         return TRIANGLE
     if kind in (CAUSAL, "causal"):
         return CAUSAL
+    if kind in (BLOCKSPARSE, "blocksparse"):
+        return BLOCKSPARSE
     raise ValueError(f"unknown kind {kind!r}")
 
 
@@ -136,6 +144,27 @@ def ta_build_schedule(kind, cu_seqlens, sink, window, last, tile, splits=0):
     _check(L.ta_build_schedule(_kind(kind), cu.ctypes.data, cu.size - 1, sink,
                                window, last, tile, splits, words.ctypes.data,
                                words.size, ctypes.byref(info)))
+    return words, info
+
+
+def ta_build_blocksparse_schedule(cu_seqlens, tile, qtile_ptr, ktile_idx,
+                                  max_tiles_per_item=0):
+    """Build a block-sparse schedule on the host from per-q-tile k-tile
+    lists in CSR form: returns (int32 words, ScheduleInfo)."""
+    L = lib()
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    ptr = np.ascontiguousarray(np.asarray(qtile_ptr, dtype=np.int32))
+    idx = np.ascontiguousarray(np.asarray(ktile_idx, dtype=np.int32))
+    idx_p = idx.ctypes.data if idx.size else None
+    info = ScheduleInfo()
+    _check(L.ta_build_blocksparse_schedule(cu.ctypes.data, cu.size - 1, tile,
+                                           ptr.ctypes.data, idx_p, max_tiles_per_item,
+                                           None, 0, ctypes.byref(info)))
+    words = np.zeros(info.words, dtype=np.int32)
+    _check(L.ta_build_blocksparse_schedule(cu.ctypes.data, cu.size - 1, tile,
+                                           ptr.ctypes.data, idx_p, max_tiles_per_item,
+                                           words.ctypes.data, words.size,
+                                           ctypes.byref(info)))
     return words, info
 
 
@@ -201,6 +230,18 @@ def triangle_attn_merge(o, lse, sched_dev, info, workspace, stream=None):
         total, hq, d, _ptr(workspace), ws_bytes, _stream(stream)))
 
 
+def blocksparse_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
+                         workspace, stream=None):
+    """Enqueue block-sparse causal attention (tiles + merge)."""
+    total, hq, d = q.shape
+    hkv = k.shape[1]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().blocksparse_attn_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
+        _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
+        float(softmax_scale), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
 def causal_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
                     stream=None):
     """Enqueue dense causal attention on ``stream``; arguments as above."""
@@ -220,11 +261,19 @@ class Plan:
     """
 
     def __init__(self, kind, cu_seqlens, sink, window, last, tile, hq,
-                 head_dim, splits=0, device="cuda"):
+                 head_dim, splits=0, device="cuda", blocks=None):
+        """blocks: (qtile_ptr, ktile_idx) for kind "blocksparse" (splits is
+        then the work bound per item)."""
         import torch
         self.kind = _kind(kind)
-        self.words, self.info = ta_build_schedule(self.kind, cu_seqlens, sink,
-                                                  window, last, tile, splits)
+        if self.kind == BLOCKSPARSE:
+            if blocks is None:
+                raise ValueError("a block-sparse plan needs blocks=(qtile_ptr, ktile_idx)")
+            self.words, self.info = ta_build_blocksparse_schedule(
+                cu_seqlens, tile, blocks[0], blocks[1], splits)
+        else:
+            self.words, self.info = ta_build_schedule(self.kind, cu_seqlens, sink,
+                                                      window, last, tile, splits)
         self.sched = torch.from_numpy(self.words).to(device)
         nbytes = ta_workspace_bytes(self.info, hq, head_dim)
         self.workspace = (torch.empty(nbytes, dtype=torch.uint8, device=device)
@@ -236,6 +285,9 @@ class Plan:
         if self.kind == TRIANGLE:
             triangle_attn_fwd(q, k, v, o, lse, self.sched, self.info,
                               softmax_scale, self.workspace, stream)
+        elif self.kind == BLOCKSPARSE:
+            blocksparse_attn_fwd(q, k, v, o, lse, self.sched, self.info,
+                                 softmax_scale, self.workspace, stream)
         else:
             causal_attn_fwd(q, k, v, o, lse, self.sched, self.info,
                             softmax_scale, stream)

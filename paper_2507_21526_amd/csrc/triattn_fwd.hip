@@ -78,6 +78,7 @@ struct MergeArgs {
     int32_t n_partial_rows;
     int32_t n_last_rows;
     int32_t o_f32;
+    int32_t kind;  // schedule kind the merge items come from
 };
 
 __device__ __forceinline__ bool header_ok(const int32_t *s, int64_t total,
@@ -692,7 +693,7 @@ template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 {
     const int32_t *sched = a.sched;
-    if (!header_ok(sched, a.total_tokens, a.n_items, TA_KIND_TRIANGLE))
+    if (!header_ok(sched, a.total_tokens, a.n_items, a.kind))
         return;
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -935,6 +936,7 @@ ta_status launch_merge(void *o, int32_t o_dtype, float *lse, const int32_t *sche
                        int32_t head_dim, const float *part_o, const float *part_lse,
                        hipStream_t stream)
 {
+    // merge items come from Triangle (Last rows) or block-sparse schedules
     if (info->n_merge_items <= 0 || info->n_last_rows <= 0)
         return TA_OK;
     MergeArgs m;
@@ -950,6 +952,7 @@ ta_status launch_merge(void *o, int32_t o_dtype, float *lse, const int32_t *sche
     m.n_partial_rows = info->n_partial_rows;
     m.n_last_rows = info->n_last_rows;
     m.o_f32 = o_dtype == TA_OUT_F32;
+    m.kind = info->kind;
     const int64_t waves = (int64_t)info->n_last_rows * hq;
     dim3 grid((unsigned)((waves + 3) / 4));
     if (head_dim == 128)
@@ -1052,6 +1055,37 @@ extern "C" ta_status triangle_attn_merge(void *o, int32_t o_dtype, float *lse,
                         part_o, part_lse, static_cast<hipStream_t>(stream));
 }
 
+namespace {
+// The two launches of a pass with split q-tiles (Triangle: Last rows;
+// block-sparse: q-tiles with several items): tiles, then merge.
+ta_status split_pass_fwd(const char *fn, int kind, const void *q, const void *k,
+                         const void *v, void *o, int32_t o_dtype, float *lse,
+                         const int32_t *sched_dev, const ta_schedule_info *info,
+                         int64_t total_tokens, int32_t hq, int32_t hkv, int32_t head_dim,
+                         float softmax_scale, void *workspace, size_t workspace_bytes,
+                         void *stream)
+{
+    clear_error();
+    ta_status st = check_common(fn, kind, q, k, v, o, o_dtype, sched_dev, info,
+                                total_tokens, hq, hkv, head_dim, softmax_scale);
+    if (st != TA_OK)
+        return st;
+    float *part_o, *part_lse;
+    st = resolve_workspace(fn, info, hq, head_dim, workspace, workspace_bytes, &part_o,
+                           &part_lse);
+    if (st != TA_OK)
+        return st;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
+                                hq, hkv, softmax_scale, part_o, part_lse);
+    st = launch_tiles(kind, a, head_dim, s);
+    if (st != TA_OK)
+        return st;
+    return launch_merge(o, o_dtype, lse, sched_dev, info, total_tokens, hq, head_dim,
+                        part_o, part_lse, s);
+}
+}  // namespace
+
 extern "C" ta_status triangle_attn_fwd(const void *q, const void *k, const void *v,
                                        void *o, int32_t o_dtype, float *lse,
                                        const int32_t *sched_dev,
@@ -1061,25 +1095,23 @@ extern "C" ta_status triangle_attn_fwd(const void *q, const void *k, const void 
                                        void *workspace, size_t workspace_bytes,
                                        void *stream)
 {
-    clear_error();
-    ta_status st = check_common("triangle_attn_fwd", TA_KIND_TRIANGLE, q, k, v, o,
-                                o_dtype, sched_dev, info, total_tokens, hq, hkv,
-                                head_dim, softmax_scale);
-    if (st != TA_OK)
-        return st;
-    float *part_o, *part_lse;
-    st = resolve_workspace("triangle_attn_fwd", info, hq, head_dim, workspace,
-                           workspace_bytes, &part_o, &part_lse);
-    if (st != TA_OK)
-        return st;
-    const hipStream_t s = static_cast<hipStream_t>(stream);
-    const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
-                                hq, hkv, softmax_scale, part_o, part_lse);
-    st = launch_tiles(TA_KIND_TRIANGLE, a, head_dim, s);
-    if (st != TA_OK)
-        return st;
-    return launch_merge(o, o_dtype, lse, sched_dev, info, total_tokens, hq, head_dim,
-                        part_o, part_lse, s);
+    return split_pass_fwd("triangle_attn_fwd", TA_KIND_TRIANGLE, q, k, v, o, o_dtype, lse,
+                          sched_dev, info, total_tokens, hq, hkv, head_dim, softmax_scale,
+                          workspace, workspace_bytes, stream);
+}
+
+extern "C" ta_status blocksparse_attn_fwd(const void *q, const void *k, const void *v,
+                                          void *o, int32_t o_dtype, float *lse,
+                                          const int32_t *sched_dev,
+                                          const ta_schedule_info *info,
+                                          int64_t total_tokens, int32_t hq, int32_t hkv,
+                                          int32_t head_dim, float softmax_scale,
+                                          void *workspace, size_t workspace_bytes,
+                                          void *stream)
+{
+    return split_pass_fwd("blocksparse_attn_fwd", TA_KIND_BLOCKSPARSE, q, k, v, o, o_dtype,
+                          lse, sched_dev, info, total_tokens, hq, hkv, head_dim,
+                          softmax_scale, workspace, workspace_bytes, stream);
 }
 
 extern "C" ta_status causal_attn_fwd(const void *q, const void *k, const void *v,

@@ -49,6 +49,50 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 using namespace triattn;
 
+namespace {
+
+// Write the packed schedule (header, split items, direct items, merges).
+void pack_schedule(int32_t *w, int32_t kind, int32_t tile, int32_t batch, int32_t sink,
+                   int32_t window, int32_t last, int32_t splits, int64_t total,
+                   const std::vector<Item> &split_items, const std::vector<Item> &items,
+                   const std::vector<Merge> &merges, int64_t partial_rows, int64_t kept,
+                   int64_t merged_rows)
+{
+    w[H_MAGIC] = TA_SCHEDULE_MAGIC;
+    w[H_VERSION] = TA_SCHEDULE_VERSION;
+    w[H_KIND] = kind;
+    w[H_TILE] = tile;
+    w[H_BATCH] = batch;
+    w[H_SINK] = sink;
+    w[H_WINDOW] = window;
+    w[H_LAST] = last;
+    w[H_SPLITS] = splits;
+    w[H_TOTAL_LO] = (int32_t)(uint32_t)((uint64_t)total & 0xffffffffu);
+    w[H_TOTAL_HI] = (int32_t)(uint32_t)((uint64_t)total >> 32);
+    w[H_ITEMS] = (int32_t)(split_items.size() + items.size());
+    w[H_MERGES] = (int32_t)merges.size();
+    w[H_PARTIAL_ROWS] = (int32_t)partial_rows;
+    w[H_KEPT_TILES] = (int32_t)kept;
+    w[H_LAST_ROWS] = (int32_t)merged_rows;
+    w += kHdrWords;
+    for (const Item &it : split_items) {
+        std::memcpy(w, it.w, sizeof it.w);
+        w += kItemWords;
+    }
+    for (const Item &it : items) {
+        std::memcpy(w, it.w, sizeof it.w);
+        w += kItemWords;
+    }
+    for (const Merge &m : merges) {
+        std::memcpy(w, m.w, sizeof m.w);
+        w += kMergeWords;
+    }
+}
+
+constexpr int32_t kBlockSparseAutoTiles = 16;  // default work bound per item
+
+}  // namespace
+
 extern "C" int32_t ta_abi_version(void) { return TA_ABI_VERSION; }
 
 extern "C" const char *ta_last_error(void) { return g_last_error.c_str(); }
@@ -203,36 +247,155 @@ extern "C" ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
                     "ta_build_schedule: out has %lld words, needs %lld",
                     (long long)out_words, (long long)words);
 
-    int32_t *w = out;
-    w[H_MAGIC] = TA_SCHEDULE_MAGIC;
-    w[H_VERSION] = TA_SCHEDULE_VERSION;
-    w[H_KIND] = kind;
-    w[H_TILE] = tile;
-    w[H_BATCH] = batch;
-    w[H_SINK] = sink;
-    w[H_WINDOW] = window;
-    w[H_LAST] = last;
-    w[H_SPLITS] = splits;
-    w[H_TOTAL_LO] = (int32_t)(uint32_t)((uint64_t)total & 0xffffffffu);
-    w[H_TOTAL_HI] = (int32_t)(uint32_t)((uint64_t)total >> 32);
-    w[H_ITEMS] = (int32_t)n_main;
-    w[H_MERGES] = (int32_t)merges.size();
-    w[H_PARTIAL_ROWS] = (int32_t)partial_rows;
-    w[H_KEPT_TILES] = (int32_t)kept;
-    w[H_LAST_ROWS] = (int32_t)last_rows_total;
-    w += kHdrWords;
-    for (const Item &it : last_items) {
-        std::memcpy(w, it.w, sizeof it.w);
-        w += kItemWords;
+    pack_schedule(out, kind, tile, batch, sink, window, last, splits, total, last_items,
+                  items, merges, partial_rows, kept, last_rows_total);
+    return TA_OK;
+}
+
+
+extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
+                                                   int32_t batch, int32_t tile,
+                                                   const int32_t *qtile_ptr,
+                                                   const int32_t *ktile_idx,
+                                                   int32_t max_tiles_per_item,
+                                                   int32_t *out, int64_t out_words,
+                                                   ta_schedule_info *info)
+{
+    clear_error();
+    static const char fn[] = "ta_build_blocksparse_schedule";
+    if (!info)
+        return fail(TA_ERR_INVALID_ARG, "%s: info is NULL", fn);
+    if (!cu_seqlens || !qtile_ptr)
+        return fail(TA_ERR_INVALID_ARG, "%s: cu_seqlens or qtile_ptr is NULL", fn);
+    if (batch < 0 || max_tiles_per_item < 0 || out_words < 0)
+        return fail(TA_ERR_INVALID_ARG,
+                    "%s: need batch >= 0, max_tiles_per_item >= 0, out_words >= 0", fn);
+    if (tile != 64 && tile != 128)
+        return fail(TA_ERR_UNSUPPORTED, "%s: tile %d not in {64, 128}", fn, tile);
+    if (cu_seqlens[0] != 0)
+        return fail(TA_ERR_INVALID_ARG, "%s: cu_seqlens[0] != 0", fn);
+    for (int32_t b = 0; b < batch; ++b)
+        if (cu_seqlens[b + 1] < cu_seqlens[b])
+            return fail(TA_ERR_INVALID_ARG, "%s: cu_seqlens decreases at %d", fn, b);
+    if (qtile_ptr[0] != 0)
+        return fail(TA_ERR_INVALID_ARG, "%s: qtile_ptr[0] != 0", fn);
+
+    const int64_t T = tile;
+    const int64_t M = max_tiles_per_item > 0 ? max_tiles_per_item : kBlockSparseAutoTiles;
+    std::vector<Item> split_items, items;
+    std::vector<Merge> merges;
+    int64_t partial_rows = 0, kept = 0, merged_rows = 0, max_splits = 0;
+    int64_t qt = 0;  // global q-tile index
+
+    for (int32_t b = 0; b < batch; ++b) {
+        const int64_t off = cu_seqlens[b];
+        const int64_t n = cu_seqlens[b + 1] - off;
+        for (int64_t t = 0; t * T < n; ++t, ++qt) {
+            const int64_t p0 = qtile_ptr[qt], p1 = qtile_ptr[qt + 1];
+            if (p1 < p0)
+                return fail(TA_ERR_INVALID_ARG, "%s: qtile_ptr decreases at q-tile %lld",
+                            fn, (long long)qt);
+            if (p1 > p0 && !ktile_idx)
+                return fail(TA_ERR_INVALID_ARG, "%s: ktile_idx is NULL", fn);
+            const int64_t r0 = t * T, r1 = std::min(r0 + T, n);
+            // pieces: maximal runs of consecutive listed k-tiles, cut at M
+            std::vector<std::pair<int64_t, int64_t>> pieces;
+            int64_t prev = -1, run0 = -1;
+            for (int64_t p = p0; p < p1; ++p) {
+                const int64_t kt = ktile_idx[p];
+                if (kt < 0 || kt > t || kt <= prev)
+                    return fail(TA_ERR_INVALID_ARG,
+                                "%s: q-tile %lld: k-tile %lld out of order or above the "
+                                "diagonal", fn, (long long)qt, (long long)kt);
+                if (run0 < 0) {
+                    run0 = kt;
+                } else if (kt != prev + 1) {
+                    for (int64_t a = run0; a <= prev; a += M)
+                        pieces.push_back({a, std::min(a + M, prev + 1)});
+                    run0 = kt;
+                }
+                prev = kt;
+            }
+            if (run0 >= 0)
+                for (int64_t a = run0; a <= prev; a += M)
+                    pieces.push_back({a, std::min(a + M, prev + 1)});
+            kept += p1 - p0;
+            // items: up to two pieces and M tiles each
+            std::vector<Item> q_items;
+            int npieces = 0;
+            for (const auto &pc : pieces) {
+                const int64_t len = pc.second - pc.first;
+                if (!q_items.empty() && npieces == 1 &&
+                    q_items.back().w[I_COST] + len <= M) {
+                    Item &it = q_items.back();
+                    it.w[I_KB0] = (int32_t)pc.first;
+                    it.w[I_KB1] = (int32_t)pc.second;
+                    it.w[I_COST] += (int32_t)len;
+                    npieces = 2;
+                    continue;
+                }
+                Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
+                            (int32_t)pc.first, (int32_t)pc.second, 0, 0, kModeCausal, -1,
+                            (int32_t)len, 0}};
+                q_items.push_back(it);
+                npieces = 1;
+            }
+            if (q_items.empty()) {  // no key for these rows: zero output
+                Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1, 0, 0, 0, 0,
+                            kModeCausal, -1, 0, 0}};
+                q_items.push_back(it);
+            }
+            if (q_items.size() == 1) {
+                items.push_back(q_items[0]);
+                continue;
+            }
+            const int64_t ns = (int64_t)q_items.size();
+            for (int64_t c = 0; c < ns; ++c) {
+                q_items[c].w[I_PART_BASE] = (int32_t)(partial_rows + c * (r1 - r0));
+                split_items.push_back(q_items[c]);
+            }
+            Merge m = {{(int32_t)off, (int32_t)r0, (int32_t)r1, (int32_t)ns,
+                        (int32_t)partial_rows, 0, 0, 0}};
+            merges.push_back(m);
+            partial_rows += ns * (r1 - r0);
+            merged_rows += r1 - r0;
+            max_splits = std::max(max_splits, ns);
+            if (partial_rows > INT32_MAX)
+                return fail(TA_ERR_UNSUPPORTED, "%s: too many partial rows", fn);
+        }
     }
-    for (const Item &it : items) {
-        std::memcpy(w, it.w, sizeof it.w);
-        w += kItemWords;
-    }
-    for (const Merge &m : merges) {
-        std::memcpy(w, m.w, sizeof m.w);
-        w += kMergeWords;
-    }
+    auto by_cost = [](const Item &a, const Item &b) { return a.w[I_COST] > b.w[I_COST]; };
+    std::stable_sort(split_items.begin(), split_items.end(), by_cost);
+    std::stable_sort(items.begin(), items.end(), by_cost);
+
+    const int64_t n_main = (int64_t)split_items.size() + (int64_t)items.size();
+    const int64_t words = kHdrWords + n_main * kItemWords +
+                          (int64_t)merges.size() * kMergeWords;
+    if (n_main > INT32_MAX / 64 || kept > INT32_MAX)
+        return fail(TA_ERR_UNSUPPORTED, "%s: schedule too large", fn);
+    const int64_t total = cu_seqlens[batch];
+    std::memset(info, 0, sizeof *info);
+    info->version = TA_SCHEDULE_VERSION;
+    info->kind = TA_KIND_BLOCKSPARSE;
+    info->tile = tile;
+    info->batch = batch;
+    info->splits_requested = max_tiles_per_item;
+    info->total_tokens = total;
+    info->words = words;
+    info->n_items = (int32_t)n_main;
+    info->n_last_items = (int32_t)split_items.size();
+    info->n_merge_items = (int32_t)merges.size();
+    info->n_last_rows = (int32_t)merged_rows;
+    info->n_partial_rows = (int32_t)partial_rows;
+    info->max_splits = (int32_t)max_splits;
+    info->kept_tiles_per_qhead = kept;
+    if (!out)
+        return TA_OK;
+    if (out_words < words)
+        return fail(TA_ERR_BUFFER_TOO_SMALL, "%s: out has %lld words, needs %lld", fn,
+                    (long long)out_words, (long long)words);
+    pack_schedule(out, TA_KIND_BLOCKSPARSE, tile, batch, 0, 0, 0, max_tiles_per_item, total,
+                  split_items, items, merges, partial_rows, kept, merged_rows);
     return TA_OK;
 }
 

@@ -24,25 +24,28 @@ def _heads(hq, hkv, seed):
     return sorted(h for h in hs if h < hq)
 
 
-def _check_workload(name, layer=0, kinds=("triangle", "causal"), n_random=96):
+def _check_workload(name, layer=0, kinds=("triangle", "causal"), n_random=96,
+                    shape=None):
+    """shape: optional (sink, window, last) replacing the workload's own."""
     w = WORKLOADS[name]
     cu = list(w.cu_seqlens)
+    sink, window, last = shape if shape else (w.sink, w.window, w.last)
     log(f"case {name} layer {layer}: drawing inputs")
     q, k, v = workload_qkv(w, layer)
     qg, kg, vg = q.cuda(), k.cuda(), v.cuda()
     heads = _heads(w.hq, w.hkv, w.seed + layer)
     for kind in kinds:
         log(f"case {name} layer {layer} {kind}: running")
-        o, lse, plan = run_pass(kind, qg, kg, vg, cu, w.sink, w.window,
-                                w.last, w.tile, poison=True)
+        o, lse, plan = run_pass(kind, qg, kg, vg, cu, sink, window, last,
+                                w.tile, poison=True)
         torch.cuda.synchronize()
         assert not torch.isnan(o).any()
-        rows = sample_rows(cu, w.sink, w.window, w.last, w.tile,
+        rows = sample_rows(cu, sink, window, last, w.tile,
                            n_random if kind == "triangle" else n_random // 2,
                            seed=w.seed + layer,
                            all_last=(kind == "triangle"))
-        compare(kind, q, k, v, cu, w.sink, w.window, w.last, w.scale, o, lse,
-                rows, heads, label=f"{name} layer {layer} {kind}")
+        compare(kind, q, k, v, cu, sink, window, last, w.scale, o, lse,
+                rows, heads, label=f"{name} layer {layer} {kind} S/W/L={sink}/{window}/{last}")
         del o, lse, plan
     del qg, kg, vg
     torch.cuda.empty_cache()
@@ -66,3 +69,14 @@ def test_qwen_stack_layers():
     dense = [l for l in range(w.layers) if l not in tri]
     _check_workload("qwen7b_n128k_stack28", tri[0], kinds=("triangle",))
     _check_workload("qwen7b_n128k_stack28", dense[0], kinds=("causal",))
+
+
+def test_llama_128k_paper_shape():
+    # the paper's own Streaming shape (sink 8, window 512; the sink is not
+    # tile aligned), timed by the benchmark next to the paper's speedup
+    _check_workload("llama8b_n128k", kinds=("triangle",), shape=(8, 512, 128))
+
+
+def test_llama_32k_streaming_only():
+    # L = 0: the Streaming pattern alone (no Last pass, no merge)
+    _check_workload("llama8b_n32k", kinds=("triangle",), shape=(128, 2048, 0))
