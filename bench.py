@@ -279,6 +279,9 @@ def timed_pass(binding, plan, q, k, v, o, scale, stream, steps, warmup, torch):
         if plan.kind == binding.TRIANGLE:
             binding.triangle_attn_fwd(q, k, v, o, None, plan.sched, plan.info, scale,
                                       plan.workspace, stream)
+        elif plan.kind == binding.BLOCKSPARSE:
+            binding.blocksparse_attn_fwd(q, k, v, o, None, plan.sched, plan.info, scale,
+                                         plan.workspace, stream)
         else:
             binding.causal_attn_fwd(q, k, v, o, None, plan.sched, plan.info, scale,
                                     stream)
@@ -300,8 +303,10 @@ def kept_flops(info, hq, tile, d):
 
 def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch):
     """Timing of the other workloads: the varlen batch (per-sequence
-    schedules), the 28-layer Qwen stack (mixed vs all-dense), and the 128K
-    Llama layer at the paper's own Streaming shape (S = 8, W = 512)."""
+    schedules), the 28-layer Qwen stack (mixed vs all-dense), block-sparse
+    causal attention on the 128K Llama layer, and that layer at the paper's
+    own Streaming shape (S = 8, W = 512)."""
+    import numpy as np
     stream = torch.cuda.current_stream()
     out = {}
 
@@ -354,6 +359,34 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         "speedup_vs_all_dense": all_dense / mixed,
         "per_layer_ms": per_layer,
     }
+
+    # block-sparse causal attention (Sec. 2.4 / 3.1, a dynamic sparse method
+    # in the dense layers): about a tenth of the causal k-tiles of each
+    # q-tile plus its diagonal tile, seeded, on the 128K Llama layer
+    w = WORKLOADS["llama8b_n128k"]
+    cu = list(w.cu_seqlens)
+    rng = np.random.default_rng(w.seed)
+    nq = -(-cu[-1] // w.tile)
+    ptr, idx = [0], []
+    for t in range(nq):
+        keep = np.flatnonzero(rng.random(t) < 0.1).tolist() + [t]
+        idx.extend(keep)
+        ptr.append(len(idx))
+    q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+    o = torch.empty_like(q)
+    bs = binding.Plan("blocksparse", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev,
+                      blocks=(ptr, idx))
+    t_bs = timed_pass(binding, bs, q, k, v, o, w.scale, stream, 5, 1, torch)
+    out["blocksparse"] = {
+        "workload": w.name, "kept_fraction_of_causal_tiles":
+            bs.info.kept_tiles_per_qhead / (nq * (nq + 1) / 2),
+        "kept_tiles_per_qhead": bs.info.kept_tiles_per_qhead,
+        "split_qtiles": bs.info.n_merge_items,
+        "ms": t_bs,
+        "kept_tile_tflops": kept_flops(bs.info, w.hq, w.tile, w.d) / t_bs / 1e9,
+        "speedup_vs_dense": (dense_128k_ms / t_bs) if dense_128k_ms else None,
+    }
+    del q, k, v, o, bs
 
     # the paper's Streaming shape on the 128K Llama layer
     w = WORKLOADS["llama8b_n128k"]
