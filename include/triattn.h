@@ -142,21 +142,21 @@ ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
  *               increasing per q-tile, each in [0, q-tile index] (tiles
  *               above the diagonal hold no key j <= i and are rejected).
  *               May be NULL when every list is empty.
- *   max_tiles_per_item  work bound per item (0 = 16): each q-tile's listed
- *               k-tiles form maximal runs of consecutive tiles; runs longer
- *               than the bound are cut into consecutive pieces of at most
- *               the bound; pieces are packed in order into items of at most
- *               two pieces and at most the bound in tiles (a piece joins the
- *               current item when it holds one piece and the sum fits).  A
+ *   max_tiles_per_item  work bound per item; 0 = automatic: max(16,
+ *               ceil(2 * listed tiles / q-tiles)), so only lists longer
+ *               than twice the mean are cut.  The list of a q-tile with m
+ *               tiles is cut, in order, into ns = max(1, ceil(m / bound))
+ *               balanced chunks (chunk c holds list entries
+ *               [c m / ns, (c + 1) m / ns)); each chunk is one work item.  A
  *               q-tile with one item writes its rows directly; one with
  *               several gets split items (normalised fp32 partials in the
  *               workspace) and a merge item, as the Last rows of Triangle
  *               attention.  Items are ordered split items first, each group
  *               by decreasing tile count (stable); merge items in q-tile
- *               order.  A q-tile with an empty list gets one item of no
- *               tile.
+ *               order.  The lists themselves are appended to the schedule.
  *   out, out_words, info  as for ta_build_schedule; info->kind is
- *               TA_KIND_BLOCKSPARSE, sink = window = last = 0 and
+ *               TA_KIND_BLOCKSPARSE, sink = last = 0, window = the number of
+ *               listed k-tiles (the length of the appended lists) and
  *               splits_requested = max_tiles_per_item.
  */
 ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens, int32_t batch,

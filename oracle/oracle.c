@@ -519,9 +519,23 @@ int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
     for (int32_t b = 0; b < batch; ++b)
         if (cu_seqlens[b + 1] < cu_seqlens[b])
             return -1;
-    const int64_t bound = max_tiles > 0 ? max_tiles : 16;
+    /* automatic bound: twice the mean list length over all q-tiles, at
+     * least 16 */
+    int64_t nq_all = 0;
+    for (int32_t b = 0; b < batch; ++b)
+        nq_all += (cu_seqlens[b + 1] - cu_seqlens[b] + tile - 1) / tile;
+    int64_t bound = max_tiles;
+    if (max_tiles == 0) {
+        const int64_t listed = qtile_ptr[nq_all] > 0 ? qtile_ptr[nq_all] : 0;
+        const int64_t nq = nq_all > 0 ? nq_all : 1;
+        bound = (2 * listed + nq - 1) / nq;
+        if (bound < 16)
+            bound = 16;
+    }
     item_vec split_items = {0}, items = {0}, merges = {0};
-    int64_t partial_rows = 0, kept_total = 0, merged_rows = 0;
+    int64_t partial_rows = 0, merged_rows = 0;
+    int32_t *kept_list = NULL; /* concatenated kept k-tiles of every q-tile */
+    int64_t kept_total = 0, kept_cap = 0;
     int fail = 0;
     int64_t g = 0; /* global q-tile */
 
@@ -543,73 +557,51 @@ int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
                 break;
             const int64_t r0 = qt * tile;
             const int64_t r1 = (r0 + tile < n) ? r0 + tile : n;
-            /* kept k-tiles by brute force over the element mask */
-            uint8_t *kept = (uint8_t *)calloc((size_t)(nkt > 0 ? nkt : 1), 1);
-            if (!kept) {
-                fail = 1;
-                break;
-            }
-            for (int64_t kt = 0; kt < nkt; ++kt) {
+            /* kept k-tiles of the q-tile by brute force over the element mask,
+             * appended in increasing order */
+            const int64_t first = kept_total;
+            for (int64_t kt = 0; kt < nkt && !fail; ++kt) {
                 const int64_t c0 = kt * tile;
                 const int64_t c1 = (c0 + tile < n) ? c0 + tile : n;
                 int any = 0;
                 for (int64_t i = r0; i < r1 && !any; ++i)
                     for (int64_t j = c0; j < c1 && !any; ++j)
                         any = oracle_bs_mask(i, j, tile, list, len);
-                kept[kt] = (uint8_t)any;
-            }
-            /* pieces: runs of kept k-tiles cut at the bound; items: up to two
-             * pieces and the bound in tiles */
-            item_vec q_items = {0};
-            int pieces_in_last = 0;
-            for (int64_t kt = 0; kt < nkt && !fail;) {
-                if (!kept[kt]) {
-                    ++kt;
+                if (!any)
                     continue;
-                }
-                int64_t e = kt;
-                while (e < nkt && kept[e])
-                    ++e;
-                for (int64_t a = kt; a < e && !fail; a += bound) {
-                    const int64_t z = (a + bound < e) ? a + bound : e;
-                    item_t *cur = q_items.n ? &q_items.v[q_items.n - 1] : NULL;
-                    if (cur && pieces_in_last == 1 && cur->w[10] + (z - a) <= bound) {
-                        cur->w[6] = (int32_t)a;
-                        cur->w[7] = (int32_t)z;
-                        cur->w[10] += (int32_t)(z - a);
-                        pieces_in_last = 2;
-                    } else {
-                        item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
-                                      (int32_t)a, (int32_t)z, 0, 0, 1, -1,
-                                      (int32_t)(z - a), 0}};
-                        fail |= push_item(&q_items, &it);
-                        pieces_in_last = 1;
+                if (kept_total == kept_cap) {
+                    kept_cap = kept_cap ? 2 * kept_cap : 1024;
+                    int32_t *nl = (int32_t *)realloc(kept_list, sizeof(int32_t) * (size_t)kept_cap);
+                    if (!nl) {
+                        fail = 1;
+                        break;
                     }
+                    kept_list = nl;
                 }
-                kt = e;
+                kept_list[kept_total++] = (int32_t)kt;
             }
-            free(kept);
-            kept_total += len;
-            if (!fail && q_items.n == 0) {
-                item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1, 0, 0,
-                              0, 0, 1, -1, 0, 0}};
-                fail |= push_item(&q_items, &it);
+            if (fail)
+                break;
+            /* balanced chunks of at most `bound` tiles, in order */
+            const int64_t m = kept_total - first;
+            int64_t ns = (m + bound - 1) / bound;
+            if (ns < 1)
+                ns = 1;
+            for (int64_t c = 0; c < ns; ++c) {
+                const int64_t a = c * m / ns, z = (c + 1) * m / ns;
+                item_t it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
+                              (int32_t)(first + a), (int32_t)(z - a), 0, 0, 2,
+                              ns > 1 ? (int32_t)(partial_rows + c * (r1 - r0)) : -1,
+                              (int32_t)(z - a), 0}};
+                fail |= push_item(ns > 1 ? &split_items : &items, &it);
             }
-            if (!fail && q_items.n == 1) {
-                fail |= push_item(&items, &q_items.v[0]);
-            } else if (!fail) {
-                const int64_t ns = q_items.n;
-                for (int64_t c = 0; c < ns; ++c) {
-                    q_items.v[c].w[9] = (int32_t)(partial_rows + c * (r1 - r0));
-                    fail |= push_item(&split_items, &q_items.v[c]);
-                }
-                item_t m = {{(int32_t)off, (int32_t)r0, (int32_t)r1, (int32_t)ns,
-                             (int32_t)partial_rows, 0, 0, 0, 0, 0, 0, 0}};
-                fail |= push_item(&merges, &m);
+            if (ns > 1) {
+                item_t mg = {{(int32_t)off, (int32_t)r0, (int32_t)r1, (int32_t)ns,
+                              (int32_t)partial_rows, 0, 0, 0, 0, 0, 0, 0}};
+                fail |= push_item(&merges, &mg);
                 partial_rows += ns * (r1 - r0);
                 merged_rows += r1 - r0;
             }
-            free(q_items.v);
         }
     }
     int64_t words = -1;
@@ -617,7 +609,7 @@ int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
         stable_sort_by_cost(&split_items);
         stable_sort_by_cost(&items);
         const int64_t n_main = split_items.n + items.n;
-        words = HDR_WORDS + n_main * ITEM_WORDS + merges.n * MERGE_WORDS;
+        words = HDR_WORDS + n_main * ITEM_WORDS + merges.n * MERGE_WORDS + kept_total;
         if (out && cap >= words) {
             const int64_t total = cu_seqlens[batch];
             int32_t *w = out;
@@ -626,7 +618,9 @@ int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
             w[2] = 2; /* block-sparse */
             w[3] = tile;
             w[4] = batch;
-            w[5] = w[6] = w[7] = 0;
+            w[5] = 0;
+            w[6] = (int32_t)kept_total; /* length of the appended lists */
+            w[7] = 0;
             w[8] = max_tiles;
             w[9] = (int32_t)(uint32_t)((uint64_t)total & 0xffffffffu);
             w[10] = (int32_t)(uint32_t)((uint64_t)total >> 32);
@@ -642,11 +636,14 @@ int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
                 memcpy(w, items.v[a].w, sizeof(int32_t) * ITEM_WORDS);
             for (int64_t a = 0; a < merges.n; ++a, w += MERGE_WORDS)
                 memcpy(w, merges.v[a].w, sizeof(int32_t) * MERGE_WORDS);
+            if (kept_total > 0)
+                memcpy(w, kept_list, sizeof(int32_t) * (size_t)kept_total);
         }
     }
     free(split_items.v);
     free(items.v);
     free(merges.v);
+    free(kept_list);
     return words;
 }
 

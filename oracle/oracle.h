@@ -97,12 +97,15 @@ int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                         const int32_t *row_head, int64_t nrows, double *out,
                         double *lse);
 /*
- * Block-sparse schedule in the packed format: kept blocks by brute force over
- * oracle_bs_mask, runs of consecutive kept k-tiles cut into pieces of at most
- * max_tiles (0 = 16), pieces packed in order into items of at most two pieces
- * and max_tiles tiles; q-tiles with several items get split items and a merge
- * item; split items first, then the rest, each stable by decreasing tiles.
- * Returns the number of words, or -1 on invalid lists.
+ * Block-sparse schedule in the packed format: the kept k-tiles of each
+ * q-tile found by brute force over oracle_bs_mask, cut in order into
+ * ns = max(1, ceil(m / bound)) balanced chunks (bound = max_tiles, or when
+ * it is 0: max(16, ceil(2 * listed tiles / q-tiles))), one
+ * list item (mode 2: ka0 = offset into the appended lists, ka1 = length)
+ * per chunk; q-tiles with several items get split items and a merge item;
+ * split items first, then the rest, each stable by decreasing tiles; the
+ * kept k-tiles of every q-tile appended in q-tile order (header word 6 holds
+ * their count).  Returns the number of words, or -1 on invalid lists.
  */
 int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
                            int32_t tile, const int32_t *qtile_ptr,

@@ -57,6 +57,8 @@ struct FwdArgs {
     int32_t hq, hkv, group;
     int32_t n_items;
     int32_t n_partial_rows;
+    int64_t list_base;    // first word of the k-tile lists (after the merges)
+    int64_t list_words;   // words in the k-tile lists
     int32_t sink, window;
     int32_t tile;
     int32_t rows_per_wg;  // R
@@ -79,6 +81,7 @@ struct MergeArgs {
     int32_t n_last_rows;
     int32_t o_f32;
     int32_t kind;  // schedule kind the merge items come from
+    int32_t tile;  // rows of a merge item are at most one q-tile
 };
 
 __device__ __forceinline__ bool header_ok(const int32_t *s, int64_t total,
@@ -234,6 +237,9 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const int32_t *sched = a.sched;
     if (!header_ok(sched, a.total_tokens, a.n_items, kind))
         return;
+    // block-sparse schedules record the length of their k-tile lists
+    if (a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0))
+        return;
 
     int bid = blockIdx.x;
     const int g = bid % a.hkv;
@@ -251,11 +257,17 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const int32_t mode = it[I_MODE];
     const int32_t part_base = it[I_PART_BASE];
     // Guard against a malformed schedule: never touch memory outside it.
+    // List items (kModeCausalList) read the k-tiles list[ka0 .. ka0 + ka1)
+    // of the tile-list section instead of two runs.
+    const bool list_mode = mode == kModeCausalList;
     if (seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
-        r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || ka1 < ka0 ||
-        kb0 < 0 || kb1 < kb0 ||
+        r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || kb0 < 0 || kb1 < kb0 ||
+        (list_mode ? (ka1 < 0 || kb1 != kb0 || (int64_t)ka0 + ka1 > a.list_words)
+                   : ka1 < ka0) ||
         (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows))
         return;
+    const int32_t *tile_list = sched + a.list_base + (list_mode ? ka0 : 0);
+    const int max_ktile = seq_len > 0 ? (seq_len - 1) / a.tile : 0;
 
     const int wr0 = r0 + sub * a.rows_per_wg;  // first row of this workgroup
     if (wr0 >= r1)
@@ -279,11 +291,16 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const int row_hi = (r1 - 1 < row_base + 31) ? r1 - 1 : row_base + 31;
     const float c = a.scale_log2;
 
-    // Steps of 64 keys over the kept k-tiles.
+    // Steps of 64 keys over the kept k-tiles: two runs, or a list (each
+    // listed index clamped to the sequence's k-tiles).
     const int tps = a.tile / kStep;
-    const int na = (ka1 - ka0) * tps;
-    const int nsteps = na + (kb1 - kb0) * tps;
+    const int na = list_mode ? ka1 * tps : (ka1 - ka0) * tps;
+    const int nsteps = list_mode ? na : na + (kb1 - kb0) * tps;
     auto step_key0 = [&](int s) -> int {
+        if (list_mode) {
+            const int kt = min(max(tile_list[s / tps], 0), max_ktile);
+            return kt * a.tile + (s % tps) * kStep;
+        }
         return s < na ? (ka0 * tps + s) * kStep : (kb0 * tps + (s - na)) * kStep;
     };
 
@@ -686,41 +703,22 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         a.lse[(int64_t)head * a.total_tokens + seq_off + my_row] = row_lse;
 }
 
-// LSE-weighted merge of the split partials of the Last rows.  One wave per
-// (Last row, query head): the wave reduces max and sum of the split LSEs
-// across its lanes, then accumulates the weighted partial rows.
+// LSE-weighted merge of the split partials of one q-tile (the Last rows of
+// Triangle attention, or a block-sparse q-tile cut into chunks).  One wave
+// per (row, query head) of merge item x: the wave reduces max and sum of the
+// split LSEs across its lanes, then accumulates the weighted partial rows.
 template <int D>
-__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
+__device__ __forceinline__ void merge_row(const MergeArgs &a, const int32_t *x, int rank,
+                                          int head, int lane)
 {
-    const int32_t *sched = a.sched;
-    if (!header_ok(sched, a.total_tokens, a.n_items, a.kind))
-        return;
-    const int lane = threadIdx.x & 63;
-    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= (int64_t)a.n_last_rows * a.hq)
-        return;
-    const int head = (int)(w % a.hq);
-    int64_t rank = w / a.hq;  // index among all Last rows
-
-    const int32_t *mi = sched + kHdrWords + (int64_t)a.n_items * kItemWords;
-    int m = 0;
-    for (; m < a.n_merges; ++m) {
-        const int32_t *x = mi + (int64_t)m * kMergeWords;
-        const int rows = x[M_R1] - x[M_R0];
-        if (rank < rows)
-            break;
-        rank -= rows;
-    }
-    if (m >= a.n_merges)
-        return;
-    const int32_t *x = mi + (int64_t)m * kMergeWords;
     const int64_t seq_off = x[M_SEQ_OFF];
     const int32_t r0 = x[M_R0], r1 = x[M_R1], ns = x[M_SPLITS], pb = x[M_PART_BASE];
     const int rows = r1 - r0;
-    if (ns < 1 || pb < 0 || pb + (int64_t)ns * rows > a.n_partial_rows ||
+    if (rows < 1 || rows > a.tile || rank >= rows || ns < 1 || pb < 0 ||
+        pb + (int64_t)ns * rows > a.n_partial_rows || seq_off < 0 || r0 < 0 ||
         seq_off + r1 > a.total_tokens)
         return;
-    const int row = r0 + (int)rank;
+    const int row = r0 + rank;
 
     auto lse_of = [&](int c) -> float {
         return a.part_lse[((int64_t)pb + (int64_t)c * rows + rank) * a.hq + head];
@@ -744,45 +742,37 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 #pragma unroll
     for (int e = 0; e < PER; ++e)
         acc[e] = 0.f;
-    // Partial rows of consecutive splits lie rows * hq * D floats apart; the
-    // loads of UNROLL splits are issued before any is used, so the wave keeps
-    // that many rows in flight (the sum still runs in split order).
+    // Partial rows of consecutive splits lie rows * hq * D floats apart.  The
+    // loads of UNROLL splits (indices clamped to the last split) are issued
+    // before any is used, so the wave keeps that many rows in flight; only
+    // the splits that exist are added, in split order.
     const int64_t split_stride = (int64_t)rows * a.hq * D;
     const float *po0 = a.part_o + (((int64_t)pb + rank) * a.hq + head) * D + PER * lane;
-    auto load_row = [&](int c, float (&t)[PER]) {
-        const float *po = po0 + (int64_t)c * split_stride;
-        if constexpr (PER == 2) {
-            const f32x2 v = *reinterpret_cast<const f32x2 *>(po);
-            t[0] = v[0];
-            t[PER - 1] = v[1];
-        } else {
-            t[0] = po[0];
-        }
-    };
     constexpr int UNROLL = 8;
-    int c = 0;
-    for (; c + UNROLL <= ns; c += UNROLL) {
+    for (int c = 0; c < ns; c += UNROLL) {
         float t[UNROLL][PER], l[UNROLL];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
-            load_row(c + u, t[u]);
-            l[u] = lse_of(c + u);
+            const int cu = min(c + u, ns - 1);
+            const float *po = po0 + (int64_t)cu * split_stride;
+            if constexpr (PER == 2) {
+                const f32x2 v = *reinterpret_cast<const f32x2 *>(po);
+                t[u][0] = v[0];
+                t[u][PER - 1] = v[1];
+            } else {
+                t[u][0] = po[0];
+            }
+            l[u] = lse_of(cu);
         }
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
-            const float wgt = __expf(l[u] - m_use);
+            if (c + u < ns) {
+                const float wgt = __expf(l[u] - m_use);
 #pragma unroll
-            for (int e = 0; e < PER; ++e)
-                acc[e] += wgt * t[u][e];
+                for (int e = 0; e < PER; ++e)
+                    acc[e] += wgt * t[u][e];
+            }
         }
-    }
-    for (; c < ns; ++c) {
-        float t[PER];
-        load_row(c, t);
-        const float wgt = __expf(lse_of(c) - m_use);
-#pragma unroll
-        for (int e = 0; e < PER; ++e)
-            acc[e] += wgt * t[e];
     }
     const float inv = den > 0.f ? 1.f / den : 0.f;
     const int64_t orow = ((seq_off + row) * a.hq + head) * (int64_t)D;
@@ -806,6 +796,25 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
     if (a.lse && lane == 0)
         a.lse[(int64_t)head * a.total_tokens + seq_off + row] =
             den > 0.f ? m_use + __logf(den) : -INFINITY;
+}
+
+// Grid: x covers the tile * hq (row, head) waves of one merge item, four per
+// workgroup; y strides over the merge items.
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
+{
+    const int32_t *sched = a.sched;
+    if (!header_ok(sched, a.total_tokens, a.n_items, a.kind) || sched[H_TILE] != a.tile)
+        return;
+    const int lane = threadIdx.x & 63;
+    const int w = (int)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (w >= a.tile * a.hq)
+        return;
+    const int head = w % a.hq;
+    const int rank = w / a.hq;  // row within the merge item
+    const int32_t *mi = sched + kHdrWords + (int64_t)a.n_items * kItemWords;
+    for (int m = blockIdx.y; m < a.n_merges; m += gridDim.y)
+        merge_row<D>(a, mi + (int64_t)m * kMergeWords, rank, head, lane);
 }
 
 // Rows per workgroup: the largest of 128, 64, 32 that divides the tile and
@@ -870,6 +879,16 @@ ta_status check_common(const char *fn, int want_kind, const void *q, const void 
     if (info->n_items < 0 || info->n_merge_items < 0 || info->n_partial_rows < 0 ||
         info->n_last_rows < 0)
         return fail(TA_ERR_SCHEDULE_MISMATCH, "%s: corrupt schedule info", fn);
+    {
+        // words = header + items + merges (+ the k-tile lists of a block-sparse
+        // schedule, whose length the window field records)
+        const int64_t base = kHdrWords + (int64_t)info->n_items * kItemWords +
+                             (int64_t)info->n_merge_items * kMergeWords;
+        const int64_t lists = want_kind == TA_KIND_BLOCKSPARSE ? info->window : 0;
+        if (lists < 0 || info->words != base + lists)
+            return fail(TA_ERR_SCHEDULE_MISMATCH, "%s: schedule words %lld do not match "
+                        "its items", fn, (long long)info->words);
+    }
     if (total_tokens > 0 || info->n_items > 0) {
         if (!q || !k || !v || !o || !sched_dev)
             return fail(TA_ERR_INVALID_ARG, "%s: NULL q, k, v, o or schedule", fn);
@@ -907,6 +926,9 @@ FwdArgs make_args(const void *q, const void *k, const void *v, void *o,
     a.group = group;
     a.n_items = info->n_items;
     a.n_partial_rows = info->n_partial_rows;
+    a.list_base = kHdrWords + (int64_t)info->n_items * kItemWords +
+                  (int64_t)info->n_merge_items * kMergeWords;
+    a.list_words = info->words - a.list_base;
     a.sink = info->sink;
     a.window = info->window;
     a.tile = info->tile;
@@ -953,8 +975,9 @@ ta_status launch_merge(void *o, int32_t o_dtype, float *lse, const int32_t *sche
     m.n_last_rows = info->n_last_rows;
     m.o_f32 = o_dtype == TA_OUT_F32;
     m.kind = info->kind;
-    const int64_t waves = (int64_t)info->n_last_rows * hq;
-    dim3 grid((unsigned)((waves + 3) / 4));
+    m.tile = info->tile;
+    dim3 grid((unsigned)((info->tile * hq + 3) / 4),
+              (unsigned)std::min<int32_t>(info->n_merge_items, 65535));
     if (head_dim == 128)
         hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, m);
     else

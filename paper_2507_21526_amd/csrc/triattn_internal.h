@@ -16,6 +16,9 @@ namespace triattn {
 //   main item (kItemWords): seq_off, seq_len, r0, r1, ka0, ka1, kb0, kb1,
 //     mode, part_base, kept k-tiles, 0.
 //   merge item (kMergeWords): seq_off, r0, r1, splits, part_base, 0, 0, 0.
+//   k-tile lists (block-sparse schedules only): int32 k-tile indices, after
+//     the merge items; a list item (mode kModeCausalList) visits
+//     lists[ka0 .. ka0 + ka1) in order.
 constexpr int kHdrWords = 16;
 constexpr int kItemWords = 12;
 constexpr int kMergeWords = 8;
@@ -34,9 +37,10 @@ enum ItemField {
 enum MergeField { M_SEQ_OFF = 0, M_R0, M_R1, M_SPLITS, M_PART_BASE };
 
 // Item masks: streaming rows keep j <= i && (j < sink || i - j < window);
-// causal rows (Last rows, dense causal) keep j <= i.
+// causal rows (Last rows, dense causal, block-sparse lists) keep j <= i.
 constexpr int kModeStreaming = 0;
 constexpr int kModeCausal = 1;
+constexpr int kModeCausalList = 2;  // causal rows over a listed set of k-tiles
 
 // Record a message for ta_last_error() and return the status.
 ta_status fail(ta_status st, const char *fmt, ...);

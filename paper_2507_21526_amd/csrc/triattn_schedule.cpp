@@ -89,7 +89,7 @@ void pack_schedule(int32_t *w, int32_t kind, int32_t tile, int32_t batch, int32_
     }
 }
 
-constexpr int32_t kBlockSparseAutoTiles = 16;  // default work bound per item
+constexpr int32_t kBlockSparseAutoTiles = 16;  // least automatic work bound
 
 }  // namespace
 
@@ -281,10 +281,20 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
         return fail(TA_ERR_INVALID_ARG, "%s: qtile_ptr[0] != 0", fn);
 
     const int64_t T = tile;
-    const int64_t M = max_tiles_per_item > 0 ? max_tiles_per_item : kBlockSparseAutoTiles;
+    // Automatic bound: only q-tiles listing more than twice the mean number
+    // of tiles are cut (and never into chunks under 16 tiles), so uniform
+    // lists stay whole and a skewed list does not set the critical path.
+    int64_t n_qtiles = 0;
+    for (int32_t b = 0; b < batch; ++b)
+        n_qtiles += ceil_div((int64_t)cu_seqlens[b + 1] - cu_seqlens[b], T);
+    const int64_t listed = std::max<int64_t>(0, qtile_ptr[n_qtiles]);
+    const int64_t M = max_tiles_per_item > 0
+                          ? max_tiles_per_item
+                          : std::max<int64_t>(kBlockSparseAutoTiles,
+                                              ceil_div(2 * listed, std::max<int64_t>(n_qtiles, 1)));
     std::vector<Item> split_items, items;
     std::vector<Merge> merges;
-    int64_t partial_rows = 0, kept = 0, merged_rows = 0, max_splits = 0;
+    int64_t partial_rows = 0, merged_rows = 0, max_splits = 0;
     int64_t qt = 0;  // global q-tile index
 
     for (int32_t b = 0; b < batch; ++b) {
@@ -297,59 +307,31 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
                             fn, (long long)qt);
             if (p1 > p0 && !ktile_idx)
                 return fail(TA_ERR_INVALID_ARG, "%s: ktile_idx is NULL", fn);
-            const int64_t r0 = t * T, r1 = std::min(r0 + T, n);
-            // pieces: maximal runs of consecutive listed k-tiles, cut at M
-            std::vector<std::pair<int64_t, int64_t>> pieces;
-            int64_t prev = -1, run0 = -1;
             for (int64_t p = p0; p < p1; ++p) {
                 const int64_t kt = ktile_idx[p];
-                if (kt < 0 || kt > t || kt <= prev)
+                if (kt < 0 || kt > t || (p > p0 && kt <= ktile_idx[p - 1]))
                     return fail(TA_ERR_INVALID_ARG,
                                 "%s: q-tile %lld: k-tile %lld out of order or above the "
                                 "diagonal", fn, (long long)qt, (long long)kt);
-                if (run0 < 0) {
-                    run0 = kt;
-                } else if (kt != prev + 1) {
-                    for (int64_t a = run0; a <= prev; a += M)
-                        pieces.push_back({a, std::min(a + M, prev + 1)});
-                    run0 = kt;
-                }
-                prev = kt;
             }
-            if (run0 >= 0)
-                for (int64_t a = run0; a <= prev; a += M)
-                    pieces.push_back({a, std::min(a + M, prev + 1)});
-            kept += p1 - p0;
-            // items: up to two pieces and M tiles each
+            if (p1 > INT32_MAX)
+                return fail(TA_ERR_UNSUPPORTED, "%s: lists too long", fn);
+            const int64_t r0 = t * T, r1 = std::min(r0 + T, n);
+            // balanced chunks of the list, at most M tiles each, in order
+            const int64_t len = p1 - p0;
+            const int64_t ns = std::max<int64_t>(1, ceil_div(len, M));
             std::vector<Item> q_items;
-            int npieces = 0;
-            for (const auto &pc : pieces) {
-                const int64_t len = pc.second - pc.first;
-                if (!q_items.empty() && npieces == 1 &&
-                    q_items.back().w[I_COST] + len <= M) {
-                    Item &it = q_items.back();
-                    it.w[I_KB0] = (int32_t)pc.first;
-                    it.w[I_KB1] = (int32_t)pc.second;
-                    it.w[I_COST] += (int32_t)len;
-                    npieces = 2;
-                    continue;
-                }
+            for (int64_t c = 0; c < ns; ++c) {
+                const int64_t a = c * len / ns, z = (c + 1) * len / ns;
                 Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
-                            (int32_t)pc.first, (int32_t)pc.second, 0, 0, kModeCausal, -1,
-                            (int32_t)len, 0}};
-                q_items.push_back(it);
-                npieces = 1;
-            }
-            if (q_items.empty()) {  // no key for these rows: zero output
-                Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1, 0, 0, 0, 0,
-                            kModeCausal, -1, 0, 0}};
+                            (int32_t)(p0 + a), (int32_t)(z - a), 0, 0, kModeCausalList,
+                            -1, (int32_t)(z - a), 0}};
                 q_items.push_back(it);
             }
-            if (q_items.size() == 1) {
+            if (ns == 1) {
                 items.push_back(q_items[0]);
                 continue;
             }
-            const int64_t ns = (int64_t)q_items.size();
             for (int64_t c = 0; c < ns; ++c) {
                 q_items[c].w[I_PART_BASE] = (int32_t)(partial_rows + c * (r1 - r0));
                 split_items.push_back(q_items[c]);
@@ -364,14 +346,15 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
                 return fail(TA_ERR_UNSUPPORTED, "%s: too many partial rows", fn);
         }
     }
+    const int64_t list_words = qtile_ptr[qt];
     auto by_cost = [](const Item &a, const Item &b) { return a.w[I_COST] > b.w[I_COST]; };
     std::stable_sort(split_items.begin(), split_items.end(), by_cost);
     std::stable_sort(items.begin(), items.end(), by_cost);
 
     const int64_t n_main = (int64_t)split_items.size() + (int64_t)items.size();
     const int64_t words = kHdrWords + n_main * kItemWords +
-                          (int64_t)merges.size() * kMergeWords;
-    if (n_main > INT32_MAX / 64 || kept > INT32_MAX)
+                          (int64_t)merges.size() * kMergeWords + list_words;
+    if (n_main > INT32_MAX / 64 || list_words > INT32_MAX / 2)
         return fail(TA_ERR_UNSUPPORTED, "%s: schedule too large", fn);
     const int64_t total = cu_seqlens[batch];
     std::memset(info, 0, sizeof *info);
@@ -379,6 +362,7 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
     info->kind = TA_KIND_BLOCKSPARSE;
     info->tile = tile;
     info->batch = batch;
+    info->window = (int32_t)list_words;
     info->splits_requested = max_tiles_per_item;
     info->total_tokens = total;
     info->words = words;
@@ -388,14 +372,17 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
     info->n_last_rows = (int32_t)merged_rows;
     info->n_partial_rows = (int32_t)partial_rows;
     info->max_splits = (int32_t)max_splits;
-    info->kept_tiles_per_qhead = kept;
+    info->kept_tiles_per_qhead = list_words;
     if (!out)
         return TA_OK;
     if (out_words < words)
         return fail(TA_ERR_BUFFER_TOO_SMALL, "%s: out has %lld words, needs %lld", fn,
                     (long long)out_words, (long long)words);
-    pack_schedule(out, TA_KIND_BLOCKSPARSE, tile, batch, 0, 0, 0, max_tiles_per_item, total,
-                  split_items, items, merges, partial_rows, kept, merged_rows);
+    pack_schedule(out, TA_KIND_BLOCKSPARSE, tile, batch, 0, (int32_t)list_words, 0,
+                  max_tiles_per_item, total, split_items, items, merges, partial_rows,
+                  list_words, merged_rows);
+    if (list_words > 0)
+        std::memcpy(out + (words - list_words), ktile_idx, sizeof(int32_t) * list_words);
     return TA_OK;
 }
 

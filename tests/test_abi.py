@@ -101,8 +101,9 @@ def _fwd(fn="triangle", info=None, total=100, hq=8, hkv=2, d=128, scale=0.1,
     L = B.lib()
     pinfo = ctypes.byref(info) if info is not None else None
     p = ctypes.c_void_p(ptr)
-    if fn == "triangle":
-        return L.triangle_attn_fwd(p, p, p, p, o_dtype, None,
+    if fn in ("triangle", "blocksparse"):
+        f = L.triangle_attn_fwd if fn == "triangle" else L.blocksparse_attn_fwd
+        return f(p, p, p, p, o_dtype, None,
                                    ctypes.c_void_p(sched), pinfo, total, hq,
                                    hkv, d, scale, ctypes.c_void_p(ws),
                                    ws_bytes, None)
@@ -137,6 +138,18 @@ def test_fwd_rejects_bad_arguments_without_launching():
     bad.tile = 32
     assert _fwd(info=bad) == B.TA_ERR_UNSUPPORTED
     assert _fwd("causal", info=cau, d=80) == B.TA_ERR_UNSUPPORTED
+    # the word count must match the items (and a block-sparse list section)
+    bad = B.ScheduleInfo.from_buffer_copy(tri)
+    bad.words += 1
+    assert _fwd(info=bad) == B.TA_ERR_SCHEDULE_MISMATCH
+    _, bs = B.ta_build_blocksparse_schedule([0, 100], 64, [0, 1, 3], [0, 0, 1], 1)
+    assert bs.window == 3
+    assert _fwd("blocksparse", info=bs, ws=0) == B.TA_ERR_WORKSPACE  # checks passed
+    assert _fwd("blocksparse", info=tri) == B.TA_ERR_SCHEDULE_MISMATCH
+    for field, delta in (("words", -1), ("window", 1), ("window", -4)):
+        bad = B.ScheduleInfo.from_buffer_copy(bs)
+        setattr(bad, field, getattr(bad, field) + delta)
+        assert _fwd("blocksparse", info=bad) == B.TA_ERR_SCHEDULE_MISMATCH, field
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -128,11 +128,13 @@ def test_oracle_full_lists_equal_causal_attention():
 # ---- schedule --------------------------------------------------------------
 
 def _items(words):
-    n_items, n_merges = words[11], words[12]
+    n_items, n_merges, n_lists = words[11], words[12], words[6]
     items = words[16:16 + 12 * n_items].reshape(-1, 12)
-    merges = words[16 + 12 * n_items:].reshape(-1, 8)
-    assert merges.shape[0] == n_merges
-    return items, merges
+    m0 = 16 + 12 * n_items
+    merges = words[m0:m0 + 8 * n_merges].reshape(-1, 8)
+    lists = words[m0 + 8 * n_merges:]
+    assert lists.size == n_lists
+    return items, merges, lists
 
 
 @pytest.mark.parametrize("max_tiles", [0, 1, 2, 5])
@@ -140,20 +142,31 @@ def test_oracle_schedule_follows_the_packing_rule(max_tiles):
     cu, tile = [0, 1000, 1000, 1700], 64
     ptr, idx = random_lists(cu, tile, 0.5, 7, diag=True)
     words = oracle.schedule_bs(cu, tile, ptr, idx, max_tiles)
-    bound = max_tiles or 16
-    items, merges = _items(words)
-    assert words[2] == 2 and words[14] == len(idx)
-    # every q-tile's items cover exactly its listed k-tiles
-    cover = {}
+    nq = sum(-(-(cu[b + 1] - cu[b]) // tile) for b in range(len(cu) - 1))
+    bound = max_tiles or max(16, -(-2 * len(idx) // nq))
+    items, merges, lists = _items(words)
+    # every listed tile meets the mask (all lie on or below the diagonal), so
+    # the appended lists are the caller's lists in q-tile order
+    assert words[2] == 2 and words[14] == len(idx) and np.array_equal(lists, idx)
+    # every q-tile's items are balanced chunks that cover its list in order
+    chunks = {}
     for it in items:
         off, n, r0, r1, ka0, ka1, kb0, kb1, mode, pb, cost, _ = (int(x) for x in it)
-        assert mode == 1 and cost == (ka1 - ka0) + (kb1 - kb0) <= bound
-        assert ka1 - ka0 >= 1 and (kb1 == kb0 or kb0 > ka1 - 1)
-        cover.setdefault((off, r0), []).extend(list(range(ka0, ka1)) + list(range(kb0, kb1)))
+        assert mode == 2 and kb0 == kb1 == 0 and cost == ka1 <= bound
+        chunks.setdefault((off, r0), []).append((ka0, ka1))
+    g = 0
     for b in range(len(cu) - 1):
-        lists = lists_of_seq(cu, tile, ptr, idx, b)
-        for t, lst in enumerate(lists):
-            assert sorted(cover.get((cu[b], t * tile), [])) == lst
+        for t, lst in enumerate(lists_of_seq(cu, tile, ptr, idx, b)):
+            mine = sorted(chunks.pop((cu[b], t * tile)))
+            assert mine[0][0] == ptr[g + t]
+            assert sum(c for _, c in mine) == len(lst)
+            for (a0, c0), (a1, _) in zip(mine, mine[1:]):
+                assert a1 == a0 + c0
+            sizes = [c for _, c in mine]
+            assert len(sizes) == max(1, -(-len(lst) // bound))
+            assert max(sizes) - min(sizes) <= 1
+        g += -(-(cu[b + 1] - cu[b]) // tile)
+    assert not chunks
     # split items: contiguous partial slots per q-tile, one merge each
     split = items[items[:, 9] >= 0]
     assert words[13] == sum(int(m[3]) * (int(m[2]) - int(m[1])) for m in merges)
@@ -167,6 +180,26 @@ def test_oracle_schedule_follows_the_packing_rule(max_tiles):
     assert np.all(items[:nsplit, 9] >= 0) and np.all(items[nsplit:, 9] < 0)
     for grp in (items[:nsplit], items[nsplit:]):
         assert np.all(np.diff(grp[:, 10]) <= 0)
+
+
+def test_automatic_bound_cuts_only_long_lists():
+    # 40 q-tiles of 64: the last lists all 40 k-tiles, the others only the
+    # diagonal, so the mean is 79 / 40 and the automatic bound is 16
+    cu, tile = [0, 40 * 64], 64
+    ptr, idx = [0], []
+    for t in range(40):
+        idx.extend(range(40) if t == 39 else [t])
+        ptr.append(len(idx))
+    words = oracle.schedule_bs(cu, tile, ptr, idx, 0)
+    assert np.array_equal(words, B.ta_build_blocksparse_schedule(cu, tile, ptr, idx, 0)[0])
+    items, merges, _ = _items(words)
+    assert len(merges) == 1 and int(merges[0][1]) == 39 * 64 and int(merges[0][3]) == 3
+    assert sorted(int(x) for x in items[:, 10]) == [1] * 39 + [13, 13, 14]
+    # uniform lists (every q-tile lists everything up to the diagonal): the
+    # longest is about twice the mean, so nothing is cut
+    ptr, idx = random_lists(cu, tile, 1.0, 0)
+    words = oracle.schedule_bs(cu, tile, ptr, idx, 0)
+    assert words[12] == 0 and words[11] == 40
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -191,16 +224,17 @@ def test_builder_matches_oracle_schedule(seed, tile, max_tiles):
 def test_builder_empty_and_full_lists():
     cu, tile = [0, 300], 64
     words, info = B.ta_build_blocksparse_schedule(cu, tile, [0] * 6, [])
-    items, merges = _items(words)
+    items, merges, lists = _items(words)
     assert info.n_items == 5 and info.n_merge_items == 0 and info.kept_tiles_per_qhead == 0
-    assert np.all(items[:, 4:8] == 0)
-    # full lists with a large bound: one causal item per q-tile
+    assert lists.size == 0 and np.all(items[:, 5:8] == 0) and np.all(items[:, 8] == 2)
+    # full lists with a large bound: one item per q-tile over its whole list
     ptr, idx = random_lists(cu, tile, 1.0, 0)
     words, info = B.ta_build_blocksparse_schedule(cu, tile, ptr, idx, 100)
-    items, _ = _items(words)
-    assert info.n_merge_items == 0
+    items, _, lists = _items(words)
+    assert info.n_merge_items == 0 and np.array_equal(lists, idx)
     for it in items:
-        assert it[4] == 0 and it[5] == (it[3] - 1) // tile + 1 and it[6] == it[7] == 0
+        qt = it[2] // tile
+        assert it[4] == ptr[qt] and it[5] == qt + 1 and it[6] == it[7] == 0
 
 
 def _status(cu, tile, ptr, idx, max_tiles=0):

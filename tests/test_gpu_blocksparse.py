@@ -78,6 +78,22 @@ def test_blocksparse_full_parity(cu, hq, hkv, d, tile, density, diag, max_tiles)
              f"blocksparse cu={cu} bound={max_tiles} splits={plan.info.n_merge_items}")
 
 
+def test_skewed_lists_split_by_the_automatic_bound():
+    # one q-tile lists every k-tile, the others only the diagonal: the
+    # automatic bound cuts that list alone into a split and a merge
+    cu, tile = [0, 40 * 64 - 17], 64
+    ptr, idx = [0], []
+    for t in range(40):
+        idx.extend(range(40) if t == 39 else [t])
+        ptr.append(len(idx))
+    log(f"case blocksparse skewed lists cu={cu} T={tile} bound=auto")
+    q, k, v = draw_qkv(cu, 8, 2, 128, 41)
+    o, lse, plan = _run_bs(q.cuda(), k.cuda(), v.cuda(), cu, tile, ptr, idx, 0)
+    assert plan.info.n_merge_items == 1
+    assert not torch.isnan(o).any() and not torch.isnan(lse).any()
+    _compare(q, k, v, cu, tile, ptr, idx, o, lse, np.arange(cu[-1]), "blocksparse skewed")
+
+
 def test_full_lists_equal_the_causal_kernel():
     # every q-tile lists every k-tile up to the diagonal and the bound keeps
     # them in one item: the same work items as the dense causal pass
