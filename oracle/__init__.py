@@ -13,7 +13,10 @@ baseline leg of the benchmark may import this package; the product path
   the documented packed int32 format;
 * block-sparse causal attention (the dense layers handed to a dynamic sparse
   method, Sec. 2.4 and Sec. 3.1): a row keeps key j iff j <= i and the
-  k-tile of j is listed for the row's q-tile.
+  k-tile of j is listed for the row's q-tile;
+* the region-contribution probe of Sec. 2.2: per head and section, the sum
+  of A_ij <dO_i, V_j> (the derivative of y with respect to the probing
+  variable theta_ij at theta = 1).
 
 This module only marshals arguments through ctypes and compiles the C file
 with gcc when no built library is present.
@@ -78,6 +81,11 @@ def load():
     lib.oracle_attn_rows_bs.restype = ctypes.c_int
     lib.oracle_bs_schedule.argtypes = [vp, i32, i32, vp, vp, i32, vp, i64]
     lib.oracle_bs_schedule.restype = i64
+    lib.oracle_region_grad.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32,
+                                       i64, i64, i64, dbl, vp, vp]
+    lib.oracle_region_grad.restype = ctypes.c_int
+    lib.oracle_region_counts.argtypes = [vp, i32, i64, i64, i64, vp]
+    lib.oracle_region_counts.restype = ctypes.c_int
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -251,4 +259,43 @@ def schedule_bs(cu_seqlens, tile, qtile_ptr, ktile_idx, max_tiles=0) -> np.ndarr
     got = lib.oracle_bs_schedule(cu.ctypes.data, cu.size - 1, tile, ptr.ctypes.data,
                                  idx.ctypes.data, max_tiles, out.ctypes.data, words)
     assert got == words
+    return out
+
+
+REGIONS = ("streaming", "middle", "last")
+
+
+def region_grad(q, k, v, dout, lse, cu_seqlens, sink, window, last, scale):
+    """Per query head and section (streaming, middle, last): the sum of
+    A_ij <dO_i, V_j> and the sum of its absolute values, fp64.
+
+    q, dout: [total, Hq, d]; k, v: [total, Hkv, d] (torch bf16 or uint16
+    bits); lse: [Hq, total] natural log (any float array; used as float64).
+    Returns (sums [Hq, 3], abs_sums [Hq, 3]).
+    """
+    qb, kb, vb, db = _bf16_bits(q), _bf16_bits(k), _bf16_bits(v), _bf16_bits(dout)
+    total, hq, d = qb.shape
+    hkv = kb.shape[1]
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    assert cu[-1] == total and db.shape == qb.shape and vb.shape == kb.shape
+    ls = np.ascontiguousarray(np.asarray(lse, dtype=np.float64))
+    assert ls.shape == (hq, total)
+    sums = np.zeros((hq, 3), dtype=np.float64)
+    abs_sums = np.zeros((hq, 3), dtype=np.float64)
+    rc = load().oracle_region_grad(qb.ctypes.data, kb.ctypes.data, vb.ctypes.data,
+                                   db.ctypes.data, ls.ctypes.data, cu.ctypes.data,
+                                   cu.size - 1, hq, hkv, d, sink, window, last,
+                                   float(scale), sums.ctypes.data, abs_sums.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_region_grad rejected the request")
+    return sums, abs_sums
+
+
+def region_counts(cu_seqlens, sink, window, last) -> np.ndarray:
+    """Pairs per head in each section (streaming, middle, last), brute force."""
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    out = np.zeros(3, dtype=np.int64)
+    if load().oracle_region_counts(cu.ctypes.data, cu.size - 1, sink, window, last,
+                                   out.ctypes.data) != 0:
+        raise ValueError("oracle_region_counts rejected the request")
     return out

@@ -278,8 +278,11 @@ int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
  *     part_base, kept k-tiles, 0.   Rows [r0, r1) are relative to the
  *     sequence start; [ka0, ka1) and [kb0, kb1) are the kept k-tiles as at
  *     most two maximal runs in increasing order (an absent run is (0, 0));
- *     mode 0 = streaming mask, 1 = causal mask; part_base -1 = the item
- *     writes the output rows, else it writes partial rows part_base + (i - r0).
+ *     mode 0 = streaming mask, 1 = causal mask, 2 = causal mask over the
+ *     k-tiles lists[ka0 .. ka0 + ka1) of the list section (block-sparse);
+ *     part_base -1 = the item writes the output rows, else it writes partial
+ *     rows part_base + (i - r0).
+ *   k-tile lists (block-sparse only): header word 6 words after the merges.
  *   merge item, 8 words: seq_off, r0, r1, splits, part_base, 0, 0, 0.
  * Triangle order: the Last split items (by sequence, q-tile, split), then the
  * streaming items (by sequence, q-tile).  Causal order: by kept k-tiles,
@@ -645,6 +648,111 @@ int64_t oracle_bs_schedule(const int32_t *cu_seqlens, int32_t batch,
     free(merges.v);
     free(kept_list);
     return words;
+}
+
+/* ---- Region-contribution probe (Sec. 2.2; sections of Appendix A.3) ----
+ *
+ * The probing variable theta multiplies the attention probabilities
+ * elementwise, A_theta = theta (.) A, and the layer output is O = A_theta V.
+ * For an upstream gradient dO = d y / d O the derivative at theta = 1 is
+ *   d y / d theta_ij = sum_c dO_ic * A_ij * V_jc = A_ij <dO_i, V_j>,
+ * and Grad(M-hat, l) is its mean over the pairs of the section M-hat.
+ */
+
+static int region_of(int64_t i, int64_t j, int64_t n, int64_t sink,
+                     int64_t window, int64_t last)
+{
+    if (oracle_in_streaming(i, j, sink, window))
+        return 0;
+    if (oracle_in_middle(i, j, n, sink, window, last))
+        return 1;
+    if (oracle_in_last(i, j, n, sink, window, last))
+        return 2;
+    return -1; /* above the diagonal: in no section */
+}
+
+int oracle_region_grad(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       const uint16_t *dout, const double *lse,
+                       const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                       int32_t hkv, int32_t d, int64_t sink, int64_t window,
+                       int64_t last, double scale, double *sums,
+                       double *abs_sums)
+{
+    if (batch < 0 || hq < 1 || hkv < 1 || hq % hkv != 0 || d < 1 || cu_seqlens[0] != 0)
+        return -1;
+    for (int32_t b = 0; b < batch; ++b)
+        if (cu_seqlens[b + 1] < cu_seqlens[b])
+            return -1;
+    const int64_t total = cu_seqlens[batch];
+    const int32_t group = hq / hkv;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int32_t h = 0; h < hq; ++h) {
+        const int32_t g = h / group;
+        double acc[3] = {0, 0, 0}, acc_abs[3] = {0, 0, 0};
+        double *qi = (double *)malloc(sizeof(double) * (size_t)d);
+        double *di = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!qi || !di) {
+            bad = 1;
+            free(qi);
+            free(di);
+            continue;
+        }
+        for (int32_t b = 0; b < batch; ++b) {
+            const int64_t off = cu_seqlens[b];
+            const int64_t n = cu_seqlens[b + 1] - off;
+            for (int64_t i = 0; i < n; ++i) {
+                const int64_t ti = off + i;
+                for (int32_t c = 0; c < d; ++c) {
+                    qi[c] = widen_bf16(q[(ti * hq + h) * d + c]);
+                    di[c] = widen_bf16(dout[(ti * hq + h) * d + c]);
+                }
+                const double lse_i = lse[(int64_t)h * total + ti];
+                for (int64_t j = 0; j <= i; ++j) {
+                    const int r = region_of(i, j, n, sink, window, last);
+                    if (r < 0)
+                        continue;
+                    const int64_t tj = off + j;
+                    double z = 0.0, gv = 0.0;
+                    for (int32_t c = 0; c < d; ++c) {
+                        z += qi[c] * widen_bf16(k[(tj * hkv + g) * d + c]);
+                        gv += di[c] * widen_bf16(v[(tj * hkv + g) * d + c]);
+                    }
+                    const double a = exp(scale * z - lse_i);
+                    acc[r] += a * gv;
+                    acc_abs[r] += fabs(a * gv);
+                }
+            }
+        }
+        for (int r = 0; r < 3; ++r) {
+            sums[h * 3 + r] = acc[r];
+            if (abs_sums)
+                abs_sums[h * 3 + r] = acc_abs[r];
+        }
+        free(qi);
+        free(di);
+    }
+    return bad ? -1 : 0;
+}
+
+int oracle_region_counts(const int32_t *cu_seqlens, int32_t batch, int64_t sink,
+                         int64_t window, int64_t last, int64_t *counts)
+{
+    if (batch < 0 || cu_seqlens[0] != 0)
+        return -1;
+    counts[0] = counts[1] = counts[2] = 0;
+    for (int32_t b = 0; b < batch; ++b) {
+        const int64_t n = cu_seqlens[b + 1] - cu_seqlens[b];
+        if (n < 0)
+            return -1;
+        for (int64_t i = 0; i < n; ++i)
+            for (int64_t j = 0; j <= i; ++j) {
+                const int r = region_of(i, j, n, sink, window, last);
+                if (r >= 0)
+                    ++counts[r];
+            }
+    }
+    return 0;
 }
 
 int oracle_num_threads(void)

@@ -97,6 +97,32 @@ int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                         const int32_t *row_head, int64_t nrows, double *out,
                         double *lse);
 /*
+ * Region-contribution probe (Sec. 2.2, Grad(M-hat, l)).  The probing
+ * variable theta scales the attention probabilities elementwise; for an
+ * upstream gradient dO of the attention output the derivative at theta = 1
+ * is A_ij <dO_i, V_j>, with A_ij = exp(scale <q_i, k_j> - lse_i).  For every
+ * query head h and section r of Appendix A.3 (0 streaming, 1 middle, 2 last;
+ * together the causal mask):
+ *   sums[h * 3 + r]     = sum over (i, j) in section r of A_ij <dO_i, V_j>
+ *   abs_sums[h * 3 + r] = sum of |A_ij <dO_i, V_j>| (may be NULL).
+ * q, dout: [total, hq, d]; k, v: [total, hkv, d] (bf16 bits); lse: [hq,
+ * total] natural log, the row normaliser to use (the causal one for a dense
+ * layer).  Grad = sums / the section's pair count (oracle_region_counts).
+ * OpenMP over heads.  Returns 0, or -1 on invalid arguments.
+ */
+int oracle_region_grad(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                       const uint16_t *dout, const double *lse,
+                       const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                       int32_t hkv, int32_t d, int64_t sink, int64_t window,
+                       int64_t last, double scale, double *sums,
+                       double *abs_sums);
+
+/* Pairs (i, j) per head in each section (streaming, middle, last), summed
+ * over the sequences, by brute force.  Returns 0, or -1 on invalid input. */
+int oracle_region_counts(const int32_t *cu_seqlens, int32_t batch, int64_t sink,
+                         int64_t window, int64_t last, int64_t *counts);
+
+/*
  * Block-sparse schedule in the packed format: the kept k-tiles of each
  * q-tile found by brute force over oracle_bs_mask, cut in order into
  * ns = max(1, ceil(m / bound)) balanced chunks (bound = max_tiles, or when

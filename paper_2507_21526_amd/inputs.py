@@ -69,6 +69,11 @@ WORKLOADS = {
         sink=128, window=4096, last=256, seed=1005, layers=28,
         triangle_layers=20,
         note="Qwen2.5-7B attention shape, 28 layers: 20 Triangle, 8 dense"),
+    "llama8b_probe_n2048": Workload(
+        "llama8b_probe_n2048", (0, 2048), hq=32, hkv=8, d=128, tile=128,
+        sink=64, window=128, last=128, seed=1006,
+        note="region-contribution probe: a ~2K-token prompt of one Llama-3.1-8B "
+             "layer, sections with si 64, sl 128, last 128 (App. A.3)"),
 }
 
 
@@ -97,6 +102,15 @@ def draw_qkv(cu_seqlens, hq: int, hkv: int, d: int, seed: int,
     if key0_boost is not None and total > 0:
         k[0] *= np.float32(key0_boost)
     return tuple(torch.from_numpy(x).to(torch.bfloat16) for x in (q, k, v))
+
+
+def draw_dout(cu_seqlens, hq: int, d: int, seed: int):
+    """Seeded bf16 upstream gradient dO [T, Hq, d] of an attention output
+    (i.i.d. N(0, 1) fp32 from numpy PCG64, rounded once to bf16)."""
+    total = int(cu_seqlens[-1])
+    rng = np.random.default_rng(int(seed))
+    g = rng.standard_normal((total, hq, d), dtype=np.float32)
+    return torch.from_numpy(g).to(torch.bfloat16)
 
 
 def workload_qkv(w: Workload, layer: int = 0):
