@@ -304,8 +304,9 @@ def kept_flops(info, hq, tile, d):
 def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch):
     """Timing of the other workloads: the varlen batch (per-sequence
     schedules), the 28-layer Qwen stack (mixed vs all-dense), block-sparse
-    causal attention on the 128K Llama layer, and that layer at the paper's
-    own Streaming shape (S = 8, W = 512)."""
+    causal attention on the 128K Llama layer, that layer at the paper's own
+    Streaming shape (S = 8, W = 512), and the region-contribution probe on a
+    Llama layer at 2K and 32K tokens."""
     import numpy as np
     stream = torch.cuda.current_stream()
     out = {}
@@ -403,6 +404,48 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         "note": "paper's 15.3x at 128K (A100, Triton vs FlashAttention) used sink 8, "
                 "window 512; its number of Last rows is not stated, 128 here",
     }
+    del q, k, v, o, ps
+
+    # region-contribution probe (Sec. 2.2): one Llama-3.1-8B layer with the
+    # probe's sections (si 64, sl 128, last 128) on the paper's ~2K-token
+    # prompt and on a 32K one; a synthetic upstream gradient dO
+    w = WORKLOADS["llama8b_probe_n2048"]
+    probe = {}
+    for n, steps in ((2048, 50), (32768, 5)):
+        cu = [0, n]
+        q, k, v = gpu_qkv(n, w.hq, w.hkv, w.d, w.seed, dev, torch)
+        dout = gpu_qkv(n, w.hq, w.hkv, w.d, w.seed + 1, dev, torch)[0]
+        plan = binding.Plan("causal", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev)
+        o = torch.empty_like(q)
+        lse = torch.empty((w.hq, n), dtype=torch.float32, device=dev)
+        plan.run(q, k, v, o, lse, w.scale, stream)
+        ws = torch.empty(binding.ta_probe_workspace_bytes(plan.info, w.hq),
+                         dtype=torch.uint8, device=dev)
+        sums = torch.empty((w.hq, 3), dtype=torch.float64, device=dev)
+
+        def run_probe():
+            binding.region_grad_probe(q, k, v, dout, lse, plan.sched, plan.info, w.scale,
+                                      w.sink, w.window, w.last, sums, ws, stream)
+        run_probe()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            run_probe()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        fl = kept_flops(plan.info, w.hq, w.tile, w.d)
+        counts = binding.ta_region_counts(cu, w.sink, w.window, w.last)
+        probe[f"n{n}"] = {
+            "cu_seqlens": cu, "ms": ms, "kept_tile_tflops": fl / ms / 1e9,
+            "frac_of_bf16_peak": fl / ms / 1e9 / PEAK_BF16_TFLOPS,
+            "grad_per_section": dict(zip(("streaming", "middle", "last"), (
+                float(x) for x in binding.ta_region_grad_mean(sums.cpu().numpy(), counts)))),
+        }
+        del q, k, v, dout, o, lse, ws, sums, plan
+    out["region_probe"] = {"workload": w.name, "sink": w.sink, "window": w.window,
+                           "last": w.last, "tile": w.tile, **probe}
     return out
 
 
@@ -416,7 +459,8 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
-                    help="skip the varlen, 28-layer stack and paper-shape timings")
+                    help="skip the varlen, 28-layer stack, block-sparse, paper-shape "
+                         "and probe timings")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy first (reference "

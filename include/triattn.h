@@ -52,9 +52,9 @@
 extern "C" {
 #endif
 
-#define TA_ABI_VERSION 1
+#define TA_ABI_VERSION 2
 #define TA_SCHEDULE_MAGIC 0x54524941
-#define TA_SCHEDULE_VERSION 1
+#define TA_SCHEDULE_VERSION 2
 
 typedef enum {
     TA_OK = 0,
@@ -249,6 +249,64 @@ ta_status blocksparse_attn_fwd(const void *q, const void *k, const void *v,
                                int32_t hq, int32_t hkv, int32_t head_dim,
                                float softmax_scale, void *workspace,
                                size_t workspace_bytes, void *stream);
+
+/*
+ * Region-contribution probe (Sec. 2.2, Grad(M-hat, l); the sections of
+ * Appendix A.3).  A probing variable theta scales the attention
+ * probabilities elementwise (A_theta = theta (.) A, O = A_theta V); for an
+ * upstream gradient dO = dy/dO of the attention output, the derivative at
+ * theta = 1 is  dy / dtheta_ij = A_ij <dO_i, V_j>.  This call sums it, for
+ * every query head h and section r (0 streaming, 1 middle, 2 last; together
+ * the causal pairs j <= i of every sequence), into
+ *   region_sums[h * 3 + r]   (fp64 device array of hq * 3 values).
+ * A_ij = exp(softmax_scale <q_i, k_j> - lse_i) is recomputed from q, k and
+ * the given row normaliser.
+ *   q, dout      [total_tokens, hq, head_dim] bf16; k, v [total_tokens, hkv,
+ *                head_dim] bf16; all 16-byte aligned.
+ *   lse          [hq, total_tokens] fp32, natural log: the causal softmax
+ *                normaliser of each row (causal_attn_fwd writes it).
+ *   sched_dev, info  a TA_KIND_CAUSAL schedule of the same cu_seqlens (its
+ *                work items are the tiles the probe visits).
+ *   sink, window, last  the sections (sink = keys j < sink, window = keys
+ *                with i - j < window, last = rows i >= n - min(last, n) of
+ *                each sequence); all >= 0.  The paper probes with 64, 128,
+ *                128 on ~2K-token prompts.
+ *   workspace    device buffer of at least ta_probe_workspace_bytes(info,
+ *                hq) bytes, 8-byte aligned (NULL when that is 0); its
+ *                contents on entry do not matter.
+ * Grad(M-hat_r, l) = sum_h region_sums[h * 3 + r] / (hq * count_r) with the
+ * pair counts of ta_region_counts (ta_region_grad_mean).  The result is
+ * deterministic (fixed reduction order).  Errors as triangle_attn_fwd.
+ */
+size_t ta_probe_workspace_bytes(const ta_schedule_info *info, int32_t hq);
+ta_status region_grad_probe(const void *q, const void *k, const void *v,
+                            const void *dout, const float *lse,
+                            const int32_t *sched_dev,
+                            const ta_schedule_info *info, int64_t total_tokens,
+                            int32_t hq, int32_t hkv, int32_t head_dim,
+                            float softmax_scale, int32_t sink, int32_t window,
+                            int32_t last, double *region_sums, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+/*
+ * Host helpers of the probe (Appendix A.3 sections; Sec. 3 layer choice).
+ * ta_region_counts: pairs (i, j) per head in each section (streaming,
+ *   middle, last), summed over the sequences of cu_seqlens[batch + 1]
+ *   (host array); counts is a host array of 3.
+ * ta_region_grad_mean: grad[r] = sum_h region_sums[h * 3 + r] / (hq *
+ *   counts[r]) (0 for an empty section); host arrays.
+ * ta_select_triangle_layers: the n_triangle layers whose middle-section
+ *   value has the smallest magnitude (ties: lower layer first), written to
+ *   layers[0 .. n_triangle) in increasing order.  Values must be finite.
+ */
+ta_status ta_region_counts(const int32_t *cu_seqlens, int32_t batch,
+                           int32_t sink, int32_t window, int32_t last,
+                           int64_t *counts);
+ta_status ta_region_grad_mean(const double *region_sums, int32_t hq,
+                              const int64_t *counts, double *grad);
+ta_status ta_select_triangle_layers(const double *grad_middle,
+                                    int32_t n_layers, int32_t n_triangle,
+                                    int32_t *layers);
 
 #ifdef __cplusplus
 }

@@ -291,7 +291,7 @@ int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
 
 enum { HDR_WORDS = 16, ITEM_WORDS = 12, MERGE_WORDS = 8 };
 static const int32_t SCHED_MAGIC = 0x54524941;
-static const int32_t SCHED_VERSION = 1;
+static const int32_t SCHED_VERSION = 2;
 
 typedef struct {
     int32_t w[ITEM_WORDS];

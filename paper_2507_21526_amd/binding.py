@@ -105,6 +105,18 @@ def lib():
                                                 pinfo]
     L.blocksparse_attn_fwd.restype = ctypes.c_int
     L.blocksparse_attn_fwd.argtypes = list(L.triangle_attn_fwd.argtypes)
+    L.ta_probe_workspace_bytes.restype = ctypes.c_size_t
+    L.ta_probe_workspace_bytes.argtypes = [pinfo, i32]
+    L.region_grad_probe.restype = ctypes.c_int
+    L.region_grad_probe.argtypes = [vp, vp, vp, vp, vp, vp, pinfo, i64, i32, i32,
+                                    i32, ctypes.c_float, i32, i32, i32, vp, vp,
+                                    ctypes.c_size_t, vp]
+    L.ta_region_counts.restype = ctypes.c_int
+    L.ta_region_counts.argtypes = [vp, i32, i32, i32, i32, vp]
+    L.ta_region_grad_mean.restype = ctypes.c_int
+    L.ta_region_grad_mean.argtypes = [vp, i32, vp, vp]
+    L.ta_select_triangle_layers.restype = ctypes.c_int
+    L.ta_select_triangle_layers.argtypes = [vp, i32, i32, vp]
     _lib = L
     return L
 
@@ -251,6 +263,58 @@ def causal_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
         _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
         float(softmax_scale), _stream(stream)))
+
+
+def ta_probe_workspace_bytes(info: ScheduleInfo, hq: int) -> int:
+    return int(lib().ta_probe_workspace_bytes(ctypes.byref(info), hq))
+
+
+def region_grad_probe(q, k, v, dout, lse, sched_dev, info, softmax_scale, sink,
+                      window, last, region_sums, workspace, stream=None):
+    """Enqueue the region-contribution probe on ``stream``.
+
+    q, dout [T, Hq, d], k/v [T, Hkv, d] bf16 cuda tensors; lse [Hq, T] fp32
+    (the causal normaliser); sched_dev/info a causal schedule; region_sums
+    float64 cuda tensor [Hq, 3] (streaming, middle, last) that receives the
+    per-head sums of A_ij <dO_i, V_j>; workspace uint8 cuda tensor of >=
+    ta_probe_workspace_bytes bytes or None.
+    """
+    total, hq, d = q.shape
+    hkv = k.shape[1]
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().region_grad_probe(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(lse), _ptr(sched_dev),
+        ctypes.byref(info), total, hq, hkv, d, float(softmax_scale), sink, window,
+        last, _ptr(region_sums), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def ta_region_counts(cu_seqlens, sink, window, last) -> np.ndarray:
+    """Pairs per head in the (streaming, middle, last) sections."""
+    cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+    out = np.zeros(3, dtype=np.int64)
+    _check(lib().ta_region_counts(cu.ctypes.data, cu.size - 1, sink, window, last,
+                                  out.ctypes.data))
+    return out
+
+
+def ta_region_grad_mean(region_sums, counts) -> np.ndarray:
+    """Grad per section from host per-head sums [Hq, 3] and the counts."""
+    sums = np.ascontiguousarray(np.asarray(region_sums, dtype=np.float64))
+    cnt = np.ascontiguousarray(np.asarray(counts, dtype=np.int64))
+    assert sums.ndim == 2 and sums.shape[1] == 3 and cnt.shape == (3,)
+    out = np.zeros(3, dtype=np.float64)
+    _check(lib().ta_region_grad_mean(sums.ctypes.data, sums.shape[0], cnt.ctypes.data,
+                                     out.ctypes.data))
+    return out
+
+
+def ta_select_triangle_layers(grad_middle, n_triangle) -> list:
+    """The n_triangle layers with the smallest |Grad(middle)|, ascending."""
+    g = np.ascontiguousarray(np.asarray(grad_middle, dtype=np.float64))
+    out = np.zeros(max(int(n_triangle), 1), dtype=np.int32)
+    _check(lib().ta_select_triangle_layers(g.ctypes.data if g.size else None, g.size,
+                                           int(n_triangle), out.ctypes.data))
+    return [int(x) for x in out[:int(n_triangle)]]
 
 
 class Plan:

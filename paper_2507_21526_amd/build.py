@@ -14,7 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libtriattn.so")
 SOURCES = [os.path.join(CSRC, "triattn_schedule.cpp"),
-           os.path.join(CSRC, "triattn_fwd.hip")]
+           os.path.join(CSRC, "triattn_fwd.hip"),
+           os.path.join(CSRC, "triattn_probe.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -106,3 +106,87 @@ def test_region_counts_of_packed_sequences_add():
     parts = [oracle.region_counts([0, n], 64, 128, 128) for n in (2048, 0, 700)]
     assert np.array_equal(oracle.region_counts([0, 2048, 2048, 2748], 64, 128, 128),
                           sum(parts))
+
+
+# ---- library host functions (no GPU) ---------------------------------------
+
+from paper_2507_21526_amd import binding as B  # noqa: E402
+
+
+@pytest.mark.parametrize("cu,S,W,L", [
+    ([0, 2048], 64, 128, 128), ([0, 0, 1, 100, 357], 3, 7, 11), ([0, 64], 80, 8, 3),
+    ([0, 90, 200], 5, 200, 0), ([0, 300], 0, 0, 10), ([0], 1, 1, 1),
+])
+def test_library_region_counts_match_oracle(cu, S, W, L):
+    assert np.array_equal(B.ta_region_counts(cu, S, W, L), oracle.region_counts(cu, S, W, L))
+
+
+def test_library_region_counts_at_128k():
+    # the 128K layer with the probe's sections, against the mask counts
+    n, S, W, L = 131072, 64, 128, 128
+    stream = oracle.mask_nnz("triangle", n, S, W, 0)
+    tri = oracle.mask_nnz("triangle", n, S, W, L)
+    causal = n * (n + 1) // 2
+    assert list(B.ta_region_counts([0, n], S, W, L)) == [stream, causal - tri, tri - stream]
+
+
+def test_region_grad_mean():
+    rng = np.random.default_rng(5)
+    sums = rng.standard_normal((8, 3))
+    counts = np.array([100, 0, 7])
+    got = B.ta_region_grad_mean(sums, counts)
+    assert got[1] == 0.0
+    assert np.allclose(got[[0, 2]], sums.sum(axis=0)[[0, 2]] / (8 * counts[[0, 2]]),
+                       rtol=1e-15, atol=0)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_select_triangle_layers_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 40))
+    g = np.round(rng.standard_normal(n), 1)  # rounding makes ties
+    for k in (0, 1, n // 2, n):
+        want = sorted(sorted(range(n), key=lambda l: (abs(g[l]), l))[:k])
+        assert B.ta_select_triangle_layers(g, k) == want
+
+
+def test_select_triangle_layers_rejects_bad_input():
+    with pytest.raises(B.TriAttnError):
+        B.ta_select_triangle_layers([0.1, float("nan")], 1)
+    with pytest.raises(B.TriAttnError):
+        B.ta_select_triangle_layers([0.1, 0.2], 3)
+
+
+def test_probe_rejects_bad_arguments_without_launching():
+    import ctypes
+    FAKE = 0x10000  # never dereferenced: every call below fails its checks first
+    _, cau = B.ta_build_schedule("causal", [0, 100], 0, 1, 0, 64)
+    _, tri = B.ta_build_schedule("triangle", [0, 100], 4, 8, 2, 64)
+    ws = B.ta_probe_workspace_bytes(cau, 8)
+    assert ws == cau.n_items * 2 * 8 * 3 * 8
+
+    def call(info=cau, total=100, hq=8, hkv=2, d=128, scale=0.1, S=4, W=8, L=2,
+             sums=FAKE, ws_ptr=FAKE, ws_bytes=ws, ptr=FAKE):
+        p = ctypes.c_void_p(ptr)
+        return B.lib().region_grad_probe(
+            p, p, p, p, p, p, ctypes.byref(info) if info is not None else None,
+            total, hq, hkv, d, scale, S, W, L, ctypes.c_void_p(sums),
+            ctypes.c_void_p(ws_ptr), ws_bytes, None)
+
+    assert call(info=None) == B.TA_ERR_INVALID_ARG
+    assert call(info=tri) == B.TA_ERR_SCHEDULE_MISMATCH
+    assert call(total=99) == B.TA_ERR_SCHEDULE_MISMATCH
+    assert call(hq=7) == B.TA_ERR_INVALID_ARG
+    assert call(hq=18) == B.TA_ERR_UNSUPPORTED
+    assert call(d=96) == B.TA_ERR_UNSUPPORTED
+    assert call(scale=0.0) == B.TA_ERR_INVALID_ARG
+    assert call(W=-1) == B.TA_ERR_INVALID_ARG
+    assert call(sums=0) == B.TA_ERR_INVALID_ARG
+    assert call(sums=FAKE + 4) == B.TA_ERR_INVALID_ARG
+    assert call(ptr=0) == B.TA_ERR_INVALID_ARG
+    assert call(ptr=FAKE + 8) == B.TA_ERR_INVALID_ARG
+    assert call(ws_ptr=0) == B.TA_ERR_WORKSPACE
+    assert call(ws_bytes=ws - 1) == B.TA_ERR_WORKSPACE
+    bad = B.ScheduleInfo.from_buffer_copy(cau)
+    bad.words += 1
+    assert call(info=bad) == B.TA_ERR_SCHEDULE_MISMATCH
