@@ -97,8 +97,9 @@ def summarize(root, workload):
     import glob
     prof = os.path.join(ROOT, "profiles")
     os.makedirs(prof, exist_ok=True)
+    steps, warmup = 20, 3
     cmd = "rocprofv3 --kernel-trace --stats --output-format csv -d <dir>/trace " \
-          f"-- python3 bench.py --workload {workload} --steps 5 --warmup 1 " \
+          f"-- python3 bench.py --workload {workload} --steps {steps} --warmup {warmup} " \
           "--no-cpu-baseline --no-extra"
     stats = glob.glob(os.path.join(root, "trace", "**", "*kernel_stats.csv"),
                       recursive=True)
@@ -135,11 +136,15 @@ def summarize(root, workload):
                         key = (m.group(1), int(r["Grid_Size_X"]) // max(wg, 1))
                         groups.setdefault(key, []).append(
                             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
-            out.write("| kernel | workgroups | calls | average ms | min ms |\n")
-            out.write("|---|---|---|---|---|\n")
+            out.write("| kernel | workgroups | calls | average ms | min ms | average of "
+                      "the timed calls ms |\n")
+            out.write("|---|---|---|---|---|---|\n")
             for (k, wgs), v in sorted(groups.items()):
+                # timed calls: the last `steps` of the Triangle pass (after
+                # `warmup`), the dense pass's calls after its one warm-up
+                tail = v[-steps:] if len(v) >= steps + warmup else v[1:] or v
                 out.write(f"| {k} | {wgs} | {len(v)} | {sum(v) / len(v):.4f} | "
-                          f"{min(v):.4f} |\n")
+                          f"{min(v):.4f} | {sum(tail) / len(tail):.4f} |\n")
             out.write("\nFor llama8b_n128k the Triangle tile pass launches "
                       "(57 Last splits + 1023 streaming q-tiles) x 2 row halves x "
                       "8 kv heads = 17280 workgroups; dense causal launches "
@@ -336,20 +341,26 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
     w = WORKLOADS["qwen7b_n128k_stack28"]
     cu = list(w.cu_seqlens)
     tri_layers = set(triangle_layer_set(w))
+    tri8_layers = set(triangle_layer_set(w, 8))  # the paper's Qwen setting
     tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
                        device=dev)
+    strm = binding.Plan("triangle", cu, w.sink, w.window, 0, w.tile, w.hq, w.d,
+                        device=dev)
     den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
                        device=dev)
-    mixed = all_dense = 0.0
+    mixed = mixed8 = stream_mix = all_dense = 0.0
     per_layer = []
     for layer in range(w.layers):
         q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed * 1000 + layer, dev, torch)
         o = torch.empty_like(q)
         t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 1, 1, torch)
-        t_use = t_den
+        t_use = t_str = t_den
         if layer in tri_layers:
             t_use = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 3, 1, torch)
+            t_str = timed_pass(binding, strm, q, k, v, o, w.scale, stream, 3, 1, torch)
         mixed += t_use
+        mixed8 += t_use if layer in tri8_layers else t_den
+        stream_mix += t_str
         all_dense += t_den
         per_layer.append(round(t_use, 3))
         del q, k, v, o
@@ -359,6 +370,11 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         "mixed_ms": mixed, "all_dense_ms": all_dense,
         "speedup_vs_all_dense": all_dense / mixed,
         "per_layer_ms": per_layer,
+        "streamingmix_ms": stream_mix,
+        "streamingmix_note": "the same 20 layers with the Streaming pattern (L = 0)",
+        "triangle8_layers": sorted(tri8_layers),
+        "mixed8_ms": mixed8,
+        "speedup8_vs_all_dense": all_dense / mixed8,
     }
 
     # block-sparse causal attention (Sec. 2.4 / 3.1, a dynamic sparse method
@@ -539,6 +555,24 @@ def main():
     tile_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     merge_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
     ms_per_step = wall * 1e3
+    step_q = np.percentile([e[0].elapsed_time(e[2]) for e in events], [25, 50, 75])
+    step_stats = {"warm_median_ms": float(step_q[1]),
+                  "warm_iqr_ms": float(step_q[2] - step_q[0])}
+    if not args.no_extra:
+        # cold steps: L2 and the 256 MB MALL flushed by a 1 GiB device write
+        # before each (same stream, so the write ends before the step starts)
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cold = []
+        for i in range(5):
+            flush.fill_(i)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            tri_step(ev)
+            cold.append(ev)
+        torch.cuda.synchronize()
+        cq = np.percentile([e[0].elapsed_time(e[2]) for e in cold], [25, 50, 75])
+        step_stats.update({"cold_median_ms": float(cq[1]), "cold_iqr_ms": float(cq[2] - cq[0]),
+                           "cold_steps": len(cold)})
+        del flush
 
     T, d = w.tile, w.d
     kept_flops = float(info.kept_tiles_per_qhead) * w.hq * 4.0 * T * T * d
@@ -609,6 +643,7 @@ def main():
             "kernel_ms": tile_ms,
         },
         "cpu_baseline": cpu,
+        "step_stats": step_stats,
         "merge": {"kernel_ms": merge_ms, "algorithmic_bytes": merge_bytes,
                   "gbs": merge_gbs, "frac_of_hbm_peak":
                   (merge_gbs / PEAK_HBM_GBS) if merge_gbs else None},

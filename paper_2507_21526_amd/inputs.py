@@ -120,10 +120,13 @@ def workload_qkv(w: Workload, layer: int = 0):
                     w.key0_boost)
 
 
-def triangle_layer_set(w: Workload) -> list:
-    """Seeded choice of which layers of a stack use Triangle attention."""
+def triangle_layer_set(w: Workload, count: int | None = None) -> list:
+    """Seeded choice of which layers of a stack use Triangle attention (the
+    first ``count`` of one seeded permutation, default the workload's
+    number, so a smaller set is a subset of a larger one)."""
     if w.layers == 1:
         return [0]
     gen = torch.Generator(device="cpu").manual_seed(int(w.seed))
     perm = torch.randperm(w.layers, generator=gen)
-    return sorted(int(x) for x in perm[: w.triangle_layers])
+    count = w.triangle_layers if count is None else count
+    return sorted(int(x) for x in perm[:count])
