@@ -292,17 +292,41 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const float c = a.scale_log2;
 
     // Steps of 64 keys over the kept k-tiles: two runs, or a list (each
-    // listed index clamped to the sequence's k-tiles).
+    // listed index clamped to the sequence's k-tiles).  The runs are trimmed
+    // to this workgroup's rows: steps whose keys all lie past its last row
+    // (causal), or, for streaming rows, before the window of its first row
+    // and outside the sink, hold no kept pair and are skipped.
     const int tps = a.tile / kStep;
-    const int na = list_mode ? ka1 * tps : (ka1 - ka0) * tps;
-    const int nsteps = list_mode ? na : na + (kb1 - kb0) * tps;
+    const int wr_last = min(wr0 + a.rows_per_wg, r1) - 1;
+    int a_lo = ka0 * tps, a_hi = ka1 * tps, b_lo = kb0 * tps, b_hi = kb1 * tps;
+    if (!list_mode) {
+        if (mode == kModeStreaming) {
+            // run b (and run a when there is no sink) holds band keys only
+            const int first = wr0 - a.window + 1;
+            const int fs = first > 0 ? first / kStep : 0;
+            if (b_hi > b_lo)
+                b_lo = min(max(b_lo, fs), b_hi);
+            else if (a.sink == 0)
+                a_lo = min(max(a_lo, fs), a_hi);
+        }
+        const int ls = wr_last / kStep + 1;  // first step past the last row
+        if (b_hi > b_lo)
+            b_hi = max(min(b_hi, ls), b_lo);
+        else
+            a_hi = max(min(a_hi, ls), a_lo);
+    }
+    const int na = list_mode ? ka1 * tps : a_hi - a_lo;
+    int nsteps = list_mode ? na : na + (b_hi - b_lo);
     auto step_key0 = [&](int s) -> int {
         if (list_mode) {
             const int kt = min(max(tile_list[s / tps], 0), max_ktile);
             return kt * a.tile + (s % tps) * kStep;
         }
-        return s < na ? (ka0 * tps + s) * kStep : (kb0 * tps + (s - na)) * kStep;
+        return s < na ? (a_lo + s) * kStep : (b_lo + (s - na)) * kStep;
     };
+    if (list_mode)  // listed tiles increase: only the last may pass the rows
+        while (nsteps > 0 && step_key0(nsteps - 1) > wr_last)
+            --nsteps;
 
     // Q fragments (B operand of S^T = K Q^T): lane holds Q[row][16s + 8h ..].
     bf16x8 qf[QK_STEPS];
