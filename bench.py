@@ -306,7 +306,8 @@ def kept_flops(info, hq, tile, d):
     return float(info.kept_tiles_per_qhead) * hq * 4.0 * tile * tile * d
 
 
-def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch):
+def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch,
+                   only=None):
     """Timing of the other workloads: the varlen batch (per-sequence
     schedules), the 28-layer Qwen stack (mixed vs all-dense), block-sparse
     causal attention on the 128K Llama layer, that layer at the paper's own
@@ -316,152 +317,161 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
     stream = torch.cuda.current_stream()
     out = {}
 
-    # variable-length packed batch
-    w = WORKLOADS["llama8b_varlen4"]
-    cu = list(w.cu_seqlens)
-    q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
-    o = torch.empty_like(q)
-    tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
-                       device=dev)
-    den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
-                       device=dev)
-    t_tri = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 10, 2, torch)
-    t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 2, 1, torch)
-    out["varlen"] = {
-        "workload": w.name, "cu_seqlens": cu,
-        "triangle_ms": t_tri, "dense_ms": t_den,
-        "triangle_kept_tile_tflops": kept_flops(tri.info, w.hq, w.tile, w.d) / t_tri / 1e9,
-        "dense_kept_tile_tflops": kept_flops(den.info, w.hq, w.tile, w.d) / t_den / 1e9,
-        "speedup_vs_dense": t_den / t_tri,
-        "ideal_kept_tile_ratio": den.info.kept_tiles_per_qhead / tri.info.kept_tiles_per_qhead,
-    }
-    del q, k, v, o, tri, den
+    def want(name):
+        return only is None or name in only
 
-    # 28-layer Qwen stack: 20 Triangle layers (seeded choice) and 8 dense
-    w = WORKLOADS["qwen7b_n128k_stack28"]
-    cu = list(w.cu_seqlens)
-    tri_layers = set(triangle_layer_set(w))
-    tri8_layers = set(triangle_layer_set(w, 8))  # the paper's Qwen setting
-    tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
-                       device=dev)
-    strm = binding.Plan("triangle", cu, w.sink, w.window, 0, w.tile, w.hq, w.d,
-                        device=dev)
-    den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
-                       device=dev)
-    mixed = mixed8 = stream_mix = all_dense = 0.0
-    per_layer = []
-    for layer in range(w.layers):
-        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed * 1000 + layer, dev, torch)
+    if want("varlen"):
+        # variable-length packed batch
+        w = WORKLOADS["llama8b_varlen4"]
+        cu = list(w.cu_seqlens)
+        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
         o = torch.empty_like(q)
-        t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 1, 1, torch)
-        t_use = t_str = t_den
-        if layer in tri_layers:
-            t_use = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 3, 1, torch)
-            t_str = timed_pass(binding, strm, q, k, v, o, w.scale, stream, 3, 1, torch)
-        mixed += t_use
-        mixed8 += t_use if layer in tri8_layers else t_den
-        stream_mix += t_str
-        all_dense += t_den
-        per_layer.append(round(t_use, 3))
-        del q, k, v, o
-    out["stack"] = {
-        "workload": w.name, "layers": w.layers,
-        "triangle_layers": sorted(tri_layers),
-        "mixed_ms": mixed, "all_dense_ms": all_dense,
-        "speedup_vs_all_dense": all_dense / mixed,
-        "per_layer_ms": per_layer,
-        "streamingmix_ms": stream_mix,
-        "streamingmix_note": "the same 20 layers with the Streaming pattern (L = 0)",
-        "triangle8_layers": sorted(tri8_layers),
-        "mixed8_ms": mixed8,
-        "speedup8_vs_all_dense": all_dense / mixed8,
-    }
-
-    # block-sparse causal attention (Sec. 2.4 / 3.1, a dynamic sparse method
-    # in the dense layers): about a tenth of the causal k-tiles of each
-    # q-tile plus its diagonal tile, seeded, on the 128K Llama layer
-    w = WORKLOADS["llama8b_n128k"]
-    cu = list(w.cu_seqlens)
-    rng = np.random.default_rng(w.seed)
-    nq = -(-cu[-1] // w.tile)
-    ptr, idx = [0], []
-    for t in range(nq):
-        keep = np.flatnonzero(rng.random(t) < 0.1).tolist() + [t]
-        idx.extend(keep)
-        ptr.append(len(idx))
-    q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
-    o = torch.empty_like(q)
-    bs = binding.Plan("blocksparse", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev,
-                      blocks=(ptr, idx))
-    t_bs = timed_pass(binding, bs, q, k, v, o, w.scale, stream, 5, 1, torch)
-    out["blocksparse"] = {
-        "workload": w.name, "kept_fraction_of_causal_tiles":
-            bs.info.kept_tiles_per_qhead / (nq * (nq + 1) / 2),
-        "kept_tiles_per_qhead": bs.info.kept_tiles_per_qhead,
-        "split_qtiles": bs.info.n_merge_items,
-        "ms": t_bs,
-        "kept_tile_tflops": kept_flops(bs.info, w.hq, w.tile, w.d) / t_bs / 1e9,
-        "speedup_vs_dense": (dense_128k_ms / t_bs) if dense_128k_ms else None,
-    }
-    del q, k, v, o, bs
-
-    # the paper's Streaming shape on the 128K Llama layer
-    w = WORKLOADS["llama8b_n128k"]
-    cu = list(w.cu_seqlens)
-    q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
-    o = torch.empty_like(q)
-    ps = binding.Plan("triangle", cu, 8, 512, w.last, w.tile, w.hq, w.d, device=dev)
-    t_ps = timed_pass(binding, ps, q, k, v, o, w.scale, stream, 10, 2, torch)
-    out["paper_shape"] = {
-        "workload": w.name, "sink": 8, "window": 512, "last": w.last, "tile": w.tile,
-        "triangle_ms": t_ps,
-        "kept_tile_tflops": kept_flops(ps.info, w.hq, w.tile, w.d) / t_ps / 1e9,
-        "speedup_vs_dense": (dense_128k_ms / t_ps) if dense_128k_ms else None,
-        "note": "paper's 15.3x at 128K (A100, Triton vs FlashAttention) used sink 8, "
-                "window 512; its number of Last rows is not stated, 128 here",
-    }
-    del q, k, v, o, ps
-
-    # region-contribution probe (Sec. 2.2): one Llama-3.1-8B layer with the
-    # probe's sections (si 64, sl 128, last 128) on the paper's ~2K-token
-    # prompt and on a 32K one; a synthetic upstream gradient dO
-    w = WORKLOADS["llama8b_probe_n2048"]
-    probe = {}
-    for n, steps in ((2048, 50), (32768, 5)):
-        cu = [0, n]
-        q, k, v = gpu_qkv(n, w.hq, w.hkv, w.d, w.seed, dev, torch)
-        dout = gpu_qkv(n, w.hq, w.hkv, w.d, w.seed + 1, dev, torch)[0]
-        plan = binding.Plan("causal", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev)
-        o = torch.empty_like(q)
-        lse = torch.empty((w.hq, n), dtype=torch.float32, device=dev)
-        plan.run(q, k, v, o, lse, w.scale, stream)
-        ws = torch.empty(binding.ta_probe_workspace_bytes(plan.info, w.hq),
-                         dtype=torch.uint8, device=dev)
-        sums = torch.empty((w.hq, 3), dtype=torch.float64, device=dev)
-
-        def run_probe():
-            binding.region_grad_probe(q, k, v, dout, lse, plan.sched, plan.info, w.scale,
-                                      w.sink, w.window, w.last, sums, ws, stream)
-        run_probe()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(steps):
-            run_probe()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / steps
-        fl = kept_flops(plan.info, w.hq, w.tile, w.d)
-        counts = binding.ta_region_counts(cu, w.sink, w.window, w.last)
-        probe[f"n{n}"] = {
-            "cu_seqlens": cu, "ms": ms, "kept_tile_tflops": fl / ms / 1e9,
-            "frac_of_bf16_peak": fl / ms / 1e9 / PEAK_BF16_TFLOPS,
-            "grad_per_section": dict(zip(("streaming", "middle", "last"), (
-                float(x) for x in binding.ta_region_grad_mean(sums.cpu().numpy(), counts)))),
+        tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        t_tri = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 10, 2, torch)
+        t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 2, 1, torch)
+        out["varlen"] = {
+            "workload": w.name, "cu_seqlens": cu,
+            "triangle_ms": t_tri, "dense_ms": t_den,
+            "triangle_kept_tile_tflops": kept_flops(tri.info, w.hq, w.tile, w.d) / t_tri / 1e9,
+            "dense_kept_tile_tflops": kept_flops(den.info, w.hq, w.tile, w.d) / t_den / 1e9,
+            "speedup_vs_dense": t_den / t_tri,
+            "ideal_kept_tile_ratio": den.info.kept_tiles_per_qhead / tri.info.kept_tiles_per_qhead,
         }
-        del q, k, v, dout, o, lse, ws, sums, plan
-    out["region_probe"] = {"workload": w.name, "sink": w.sink, "window": w.window,
-                           "last": w.last, "tile": w.tile, **probe}
+        del q, k, v, o, tri, den
+
+    if want("stack"):
+        # 28-layer Qwen stack: 20 Triangle layers (seeded choice) and 8 dense
+        w = WORKLOADS["qwen7b_n128k_stack28"]
+        cu = list(w.cu_seqlens)
+        tri_layers = set(triangle_layer_set(w))
+        tri8_layers = set(triangle_layer_set(w, 8))  # the paper's Qwen setting
+        tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        strm = binding.Plan("triangle", cu, w.sink, w.window, 0, w.tile, w.hq, w.d,
+                            device=dev)
+        den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        mixed = mixed8 = stream_mix = all_dense = 0.0
+        per_layer = []
+        for layer in range(w.layers):
+            q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed * 1000 + layer, dev, torch)
+            o = torch.empty_like(q)
+            t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 1, 1, torch)
+            t_use = t_str = t_den
+            if layer in tri_layers:
+                t_use = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 3, 1, torch)
+                t_str = timed_pass(binding, strm, q, k, v, o, w.scale, stream, 3, 1, torch)
+            mixed += t_use
+            mixed8 += t_use if layer in tri8_layers else t_den
+            stream_mix += t_str
+            all_dense += t_den
+            per_layer.append(round(t_use, 3))
+            del q, k, v, o
+        out["stack"] = {
+            "workload": w.name, "layers": w.layers,
+            "triangle_layers": sorted(tri_layers),
+            "mixed_ms": mixed, "all_dense_ms": all_dense,
+            "speedup_vs_all_dense": all_dense / mixed,
+            "per_layer_ms": per_layer,
+            "streamingmix_ms": stream_mix,
+            "streamingmix_note": "the same 20 layers with the Streaming pattern (L = 0)",
+            "triangle8_layers": sorted(tri8_layers),
+            "mixed8_ms": mixed8,
+            "speedup8_vs_all_dense": all_dense / mixed8,
+        }
+
+    if want("blocksparse"):
+        # block-sparse causal attention (Sec. 2.4 / 3.1, a dynamic sparse method
+        # in the dense layers): about a tenth of the causal k-tiles of each
+        # q-tile plus its diagonal tile, seeded, on the 128K Llama layer
+        w = WORKLOADS["llama8b_n128k"]
+        cu = list(w.cu_seqlens)
+        rng = np.random.default_rng(w.seed)
+        nq = -(-cu[-1] // w.tile)
+        ptr, idx = [0], []
+        for t in range(nq):
+            keep = np.flatnonzero(rng.random(t) < 0.1).tolist() + [t]
+            idx.extend(keep)
+            ptr.append(len(idx))
+        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        o = torch.empty_like(q)
+        bs = binding.Plan("blocksparse", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev,
+                          blocks=(ptr, idx))
+        t_bs = timed_pass(binding, bs, q, k, v, o, w.scale, stream, 5, 1, torch)
+        out["blocksparse"] = {
+            "workload": w.name, "kept_fraction_of_causal_tiles":
+                bs.info.kept_tiles_per_qhead / (nq * (nq + 1) / 2),
+            "kept_tiles_per_qhead": bs.info.kept_tiles_per_qhead,
+            "split_qtiles": bs.info.n_merge_items,
+            "ms": t_bs,
+            "kept_tile_tflops": kept_flops(bs.info, w.hq, w.tile, w.d) / t_bs / 1e9,
+            "speedup_vs_dense": (dense_128k_ms / t_bs) if dense_128k_ms else None,
+        }
+        del q, k, v, o, bs
+
+    if want("paper_shape"):
+        # the paper's Streaming shape on the 128K Llama layer
+        w = WORKLOADS["llama8b_n128k"]
+        cu = list(w.cu_seqlens)
+        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        o = torch.empty_like(q)
+        ps = binding.Plan("triangle", cu, 8, 512, w.last, w.tile, w.hq, w.d, device=dev)
+        t_ps = timed_pass(binding, ps, q, k, v, o, w.scale, stream, 10, 2, torch)
+        out["paper_shape"] = {
+            "workload": w.name, "sink": 8, "window": 512, "last": w.last, "tile": w.tile,
+            "triangle_ms": t_ps,
+            "kept_tile_tflops": kept_flops(ps.info, w.hq, w.tile, w.d) / t_ps / 1e9,
+            "speedup_vs_dense": (dense_128k_ms / t_ps) if dense_128k_ms else None,
+            "note": "paper's 15.3x at 128K (A100, Triton vs FlashAttention) used sink 8, "
+                    "window 512; its number of Last rows is not stated, 128 here",
+        }
+        del q, k, v, o, ps
+
+    if want("region_probe"):
+        # region-contribution probe (Sec. 2.2): one Llama-3.1-8B layer with the
+        # probe's sections (si 64, sl 128, last 128) on the paper's ~2K-token
+        # prompt and on a 32K one; a synthetic upstream gradient dO
+        w = WORKLOADS["llama8b_probe_n2048"]
+        probe = {}
+        for n, steps in ((2048, 50), (32768, 5)):
+            cu = [0, n]
+            q, k, v = gpu_qkv(n, w.hq, w.hkv, w.d, w.seed, dev, torch)
+            dout = gpu_qkv(n, w.hq, w.hkv, w.d, w.seed + 1, dev, torch)[0]
+            plan = binding.Plan("causal", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev)
+            o = torch.empty_like(q)
+            lse = torch.empty((w.hq, n), dtype=torch.float32, device=dev)
+            plan.run(q, k, v, o, lse, w.scale, stream)
+            ws = torch.empty(binding.ta_probe_workspace_bytes(plan.info, w.hq),
+                             dtype=torch.uint8, device=dev)
+            sums = torch.empty((w.hq, 3), dtype=torch.float64, device=dev)
+
+            def run_probe():
+                binding.region_grad_probe(q, k, v, dout, lse, plan.sched, plan.info, w.scale,
+                                          w.sink, w.window, w.last, sums, ws, stream)
+            run_probe()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(steps):
+                run_probe()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / steps
+            fl = kept_flops(plan.info, w.hq, w.tile, w.d)
+            counts = binding.ta_region_counts(cu, w.sink, w.window, w.last)
+            probe[f"n{n}"] = {
+                "cu_seqlens": cu, "ms": ms, "kept_tile_tflops": fl / ms / 1e9,
+                "frac_of_bf16_peak": fl / ms / 1e9 / PEAK_BF16_TFLOPS,
+                "grad_per_section": dict(zip(("streaming", "middle", "last"), (
+                    float(x) for x in binding.ta_region_grad_mean(sums.cpu().numpy(), counts)))),
+            }
+            del q, k, v, dout, o, lse, ws, sums, plan
+        out["region_probe"] = {"workload": w.name, "sink": w.sink, "window": w.window,
+                               "last": w.last, "tile": w.tile, **probe}
+
     return out
 
 
@@ -477,6 +487,10 @@ def main():
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the varlen, 28-layer stack, block-sparse, paper-shape "
                          "and probe timings")
+    ap.add_argument("--section", choices=["varlen", "stack", "blocksparse", "paper_shape",
+                                          "region_probe"],
+                    help="run only this one of the other-workload timings (no headline "
+                         "step) and print its record; for profiling one kernel")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy first (reference "
@@ -503,10 +517,18 @@ def main():
     from paper_2507_21526_amd import binding
     from paper_2507_21526_amd.inputs import WORKLOADS, triangle_layer_set, workload_qkv
 
-    w = WORKLOADS[args.workload]
-    assert w.layers == 1, "the benchmark times one attention layer"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.section:
+        log(f"timing only the {args.section} section")
+        rec = extra_sections(binding, WORKLOADS, triangle_layer_set, None, dev, torch,
+                             only={args.section})
+        print(json.dumps({"section": args.section, **rec[args.section],
+                          "device": torch.cuda.get_device_name(dev)}), flush=True)
+        return
+
+    w = WORKLOADS[args.workload]
+    assert w.layers == 1, "the benchmark times one attention layer"
     log(f"drawing inputs for {w.name}")
     q, k, v = workload_qkv(w)
     qg, kg, vg = q.to(dev), k.to(dev), v.to(dev)
