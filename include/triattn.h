@@ -10,7 +10,11 @@
  * stay dense.  The forward passes follow the split structure of Appendix A.1
  * (Algorithm "Fused Triangle Attention"): streaming q-tiles over their sink
  * and window k-tiles, the Last rows split over the key range, and an
- * LSE-weighted merge of the split partials.
+ * LSE-weighted merge of the split partials.  The library also runs
+ * block-sparse causal attention over caller-listed k-tiles (the dense layers
+ * handed to a dynamic sparse method, Sec. 2.4 and 3.1) and the
+ * region-contribution probe that chooses the Triangle layers (Sec. 2.2 and
+ * 3).
  *
  * Conventions
  *   - Rows i and keys j are 0-indexed within a sequence of length n.  A
