@@ -314,6 +314,8 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
     Streaming shape (S = 8, W = 512), and the region-contribution probe on a
     Llama layer at 2K and 32K tokens."""
     import numpy as np
+
+    from paper_2507_21526_amd.inputs import blocksparse_lists
     stream = torch.cuda.current_stream()
     out = {}
 
@@ -389,13 +391,8 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         # q-tile plus its diagonal tile, seeded, on the 128K Llama layer
         w = WORKLOADS["llama8b_n128k"]
         cu = list(w.cu_seqlens)
-        rng = np.random.default_rng(w.seed)
         nq = -(-cu[-1] // w.tile)
-        ptr, idx = [0], []
-        for t in range(nq):
-            keep = np.flatnonzero(rng.random(t) < 0.1).tolist() + [t]
-            idx.extend(keep)
-            ptr.append(len(idx))
+        ptr, idx = blocksparse_lists(nq, 0.1, w.seed)
         q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
         o = torch.empty_like(q)
         bs = binding.Plan("blocksparse", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev,

@@ -113,6 +113,21 @@ def draw_dout(cu_seqlens, hq: int, d: int, seed: int):
     return torch.from_numpy(g).to(torch.bfloat16)
 
 
+def blocksparse_lists(n_qtiles: int, density: float, seed: int):
+    """Seeded per-q-tile k-tile lists in CSR form (qtile_ptr, ktile_idx) for
+    one sequence, standing in for a dynamic sparse method's block estimate:
+    q-tile t keeps each earlier k-tile with probability ``density`` (one
+    uniform draw per (t, k-tile), numpy PCG64) and always its diagonal tile,
+    as block estimators do."""
+    rng = np.random.default_rng(int(seed))
+    ptr, idx = [0], []
+    for t in range(n_qtiles):
+        keep = np.flatnonzero(rng.random(t) < density).tolist() + [t]
+        idx.extend(keep)
+        ptr.append(len(idx))
+    return ptr, idx
+
+
 def workload_qkv(w: Workload, layer: int = 0):
     """Inputs of one layer of a workload (layer l of a stack: seed*1000 + l)."""
     seed = w.seed if w.layers == 1 else w.seed * 1000 + layer

@@ -9,7 +9,7 @@ import torch
 
 import oracle
 from paper_2507_21526_amd import binding as B
-from paper_2507_21526_amd.inputs import draw_qkv
+from paper_2507_21526_amd.inputs import WORKLOADS, blocksparse_lists, draw_qkv, workload_qkv
 from tests.parity import LSE_ABS, MAX_ABS, REL_L2, log, run_pass
 from tests.test_blocksparse import random_lists
 
@@ -125,3 +125,27 @@ def test_blocksparse_32k_sampled():
                                      np.arange(0, 32768, 4096), [32767]]))
     _compare(q, k, v, cu, tile, ptr, idx, o, lse, toks,
              f"blocksparse 32K kept tiles {plan.info.kept_tiles_per_qhead}")
+
+
+def test_blocksparse_128k_bench_config():
+    # the benchmark's configuration: the 128K Llama layer with about a tenth
+    # of each q-tile's causal k-tiles plus its diagonal (the same seeded
+    # lists), automatic work bound; sampled rows, including rows of the
+    # q-tiles the bound split (merged rows) and q-tile edges
+    w = WORKLOADS["llama8b_n128k"]
+    cu, tile = list(w.cu_seqlens), w.tile
+    nq = -(-cu[-1] // tile)
+    ptr, idx = blocksparse_lists(nq, 0.1, w.seed)
+    log(f"case blocksparse 128K bench config, {len(idx)} listed tiles")
+    q, k, v = workload_qkv(w)
+    o, lse, plan = _run_bs(q.cuda(), k.cuda(), v.cuda(), cu, tile, ptr, idx, 0)
+    words = plan.words
+    m0 = 16 + 12 * plan.info.n_items
+    merges = words[m0:m0 + 8 * plan.info.n_merge_items].reshape(-1, 8)
+    assert len(merges) > 0
+    rng = np.random.default_rng(80)
+    split_rows = [int(m[1]) + r for m in merges[:: max(1, len(merges) // 4)] for r in (0, 77, 127)]
+    toks = np.unique(np.concatenate([rng.integers(0, cu[-1], 128), split_rows,
+                                     [0, 127, 128, 65535, 65536, cu[-1] - 1]]))
+    _compare(q, k, v, cu, tile, ptr, idx, o, lse, toks,
+             f"blocksparse 128K, {len(merges)} split q-tiles")
