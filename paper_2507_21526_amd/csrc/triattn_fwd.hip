@@ -235,12 +235,6 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     __shared__ __attribute__((aligned(1024))) unsigned char smem[N_STAGES * STAGE_BYTES];
 
     const int32_t *sched = a.sched;
-    if (!header_ok(sched, a.total_tokens, a.n_items, kind))
-        return;
-    // block-sparse schedules record the length of their k-tile lists
-    if (a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0))
-        return;
-
     int bid = blockIdx.x;
     const int g = bid % a.hkv;
     bid /= a.hkv;
@@ -248,6 +242,9 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const int item = bid / a.subtiles;
     if (item >= a.n_items)
         return;
+    // The item words are read before the header is checked so that both
+    // scalar loads are in flight together (the host has checked that the
+    // schedule holds n_items items, so the read is in bounds either way).
     const int32_t *it = sched + kHdrWords + (int64_t)item * kItemWords;
     const int64_t seq_off = it[I_SEQ_OFF];
     const int32_t seq_len = it[I_SEQ_LEN];
@@ -256,6 +253,11 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const int32_t kb0 = it[I_KB0], kb1 = it[I_KB1];
     const int32_t mode = it[I_MODE];
     const int32_t part_base = it[I_PART_BASE];
+    if (!header_ok(sched, a.total_tokens, a.n_items, kind))
+        return;
+    // block-sparse schedules record the length of their k-tile lists
+    if (a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0))
+        return;
     // Guard against a malformed schedule: never touch memory outside it.
     // List items (kModeCausalList) read the k-tiles list[ka0 .. ka0 + ka1)
     // of the tile-list section instead of two runs.
@@ -675,6 +677,51 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const float l_tot = pair_sum(l_run);
     const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
     const float row_lse = l_tot > 0.f ? (m_ref + __log2f(l_tot)) * kLn2 : -INFINITY;
+
+    if (part_base < 0 && !a.o_f32) {
+        // bf16 output rows, written whole: a lane holds 4-value pieces of
+        // its row spread over the row, so the wave first stages its 32 x D
+        // tile in its own slice of the (now idle) K/V stages, XOR-swizzled
+        // by 16-byte chunk, then stores complete rows.  Every wave has
+        // passed the last barrier of the loop, after which no LDS read or
+        // copy of the loop is outstanding.
+        constexpr int ROWB = D * 2;    // bytes per output row
+        constexpr int CHK = ROWB / 16; // 16-byte chunks per row
+        static_assert(NW * 32 * ROWB <= N_STAGES * STAGE_BYTES, "epilogue tile fits the stages");
+        unsigned char *tile = smem + wave * (32 * ROWB);
+        auto oswz = [](int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
+#pragma unroll
+        for (int b = 0; b < D_BLOCKS; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                f32x4 t;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    t[e] = oacc[b][4 * j + e] * inv;
+                // values d = 32 b + 8 j + 4 half + e: chunk 4 b + j, half h
+                const int pc = (4 * b + j) ^ oswz(col);
+                *reinterpret_cast<bf16x4 *>(tile + col * ROWB + pc * 16 + half * 8) =
+                    __builtin_convertvector(t, bf16x4);
+            }
+        // this wave's LDS writes complete before it reads other lanes' data
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        asm volatile("" ::: "memory");
+        __bf16 *obase = reinterpret_cast<__bf16 *>(a.o);
+#pragma unroll
+        for (int k = 0; k < 32 * CHK / 64; ++k) {
+            const int rr = lane / CHK + k * (64 / CHK);
+            const int c = lane % CHK;
+            const u32x4 val =
+                *reinterpret_cast<const u32x4 *>(tile + rr * ROWB + ((c ^ oswz(rr)) << 4));
+            if (row_base + rr < r1)
+                *reinterpret_cast<u32x4 *>(
+                    obase + ((seq_off + row_base + rr) * a.hq + head) * (int64_t)D + c * 8) = val;
+        }
+        if (a.lse && half == 0 && row_valid)
+            a.lse[(int64_t)head * a.total_tokens + seq_off + my_row] = row_lse;
+        return;
+    }
     if (!row_valid)
         return;
 
