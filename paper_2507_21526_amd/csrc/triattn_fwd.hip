@@ -232,7 +232,12 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     constexpr int COPY_STRIDE = MFMA_SLOTS / (2 * COPIES) > 0
                                     ? MFMA_SLOTS / (2 * COPIES) : 1;
 
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[N_STAGES * STAGE_BYTES];
+    // LDS: the two K/V stages, then one 32-row Q tile per wave (the prologue
+    // stages Q there so that it is read from HBM in whole rows).
+    constexpr int QTILE_BYTES = 32 * ROW_BYTES;
+    constexpr int QREGION = N_STAGES * STAGE_BYTES;
+    __shared__ __attribute__((aligned(1024))) unsigned char
+        smem[N_STAGES * STAGE_BYTES + NW * QTILE_BYTES];
 
     const int32_t *sched = a.sched;
     int bid = blockIdx.x;
@@ -331,14 +336,33 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
             --nsteps;
 
     // Q fragments (B operand of S^T = K Q^T): lane holds Q[row][16s + 8h ..].
-    bf16x8 qf[QK_STEPS];
+    // The wave's 32 Q rows are first copied whole into its LDS Q tile (1 KB
+    // per copy = 1024 / ROW_BYTES rows; lane l lands at byte 16 l: row
+    // l / CHUNKS of the copy, stored chunk l % CHUNKS holding logical chunk
+    // (l % CHUNKS) ^ kswz(row)), then read in fragment order after the
+    // prologue barrier.  Rows past the q-tile repeat its last row.
+    const uint32_t smem_addr =
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+    const int q_row0 = min(row_base, r1 - 1);  // the wave's first row to read
     {
-        const uint16_t *qp = a.q + ((seq_off + load_row) * a.hq + head) * (int64_t)D +
-                             8 * half;
+        const uint16_t *qb = a.q + ((seq_off + q_row0) * a.hq + head) * (int64_t)D;
+        const uint32_t q_pitch = (uint32_t)(a.hq * ROW_BYTES);
+#pragma unroll
+        for (int i = 0; i < QTILE_BYTES / 1024; ++i) {
+            const int row = i * (1024 / ROW_BYTES) + lane / CHUNKS;
+            const int rr = min(row_base + row, r1 - 1) - q_row0;  // 0 .. 31
+            const uint32_t off = __umul24((uint32_t)rr, q_pitch) +
+                                 (uint32_t)(((lane % CHUNKS) ^ kswz<D>(row)) << 4);
+            copy_to_lds16(qb, off, smem_addr + QREGION + wave * QTILE_BYTES + i * 1024);
+        }
+    }
+    bf16x8 qf[QK_STEPS];
+    auto read_q = [&]() {
+        const unsigned char *qt = smem + QREGION + wave * QTILE_BYTES + col * ROW_BYTES;
 #pragma unroll
         for (int s = 0; s < QK_STEPS; ++s)
-            qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
-    }
+            qf[s] = *reinterpret_cast<const bf16x8 *>(qt + (((2 * s + half) ^ kswz<D>(col)) << 4));
+    };
 
     const uint16_t *kbase = a.k + (seq_off * a.hkv + g) * (int64_t)D;
     const uint16_t *vbase = a.v + (seq_off * a.hkv + g) * (int64_t)D;
@@ -361,8 +385,6 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     // Keys past the end of the sequence are read from its last row: they lie
     // beyond every row of the item, so the causal mask gives them p = 0.
     const int key_max = seq_len - 1;
-    const uint32_t smem_addr =
-        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
 
     // One tile copy (K or V of one step into one stage).  Row r of the tile
     // reads key min(key0 + r, last key of the sequence), so a step past the
@@ -633,7 +655,8 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
             for (int c = 0; c < COPIES; ++c)
                 issue_slot(c);
         }
-        end_phase(true);
+        end_phase(true);  // K(0) and every wave's Q tile have landed
+        read_q();
         if (group == 0) {
             // j = 0: QK only, then the copies of the PV slots.
             plan_step_copies(0);
@@ -670,6 +693,8 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
             do_m(nsteps, false, true, no_hook);
             end_phase(false);
         }
+    } else {
+        wait_vmcnt(0);  // no steps: the Q copies must still land before exit
     }
 
     if (!wave_active)
