@@ -69,6 +69,11 @@ WORKLOADS = {
         sink=128, window=4096, last=256, seed=1005, layers=28,
         triangle_layers=20,
         note="Qwen2.5-7B attention shape, 28 layers: 20 Triangle, 8 dense"),
+    "triangle_n1m_g8": Workload(
+        "triangle_n1m_g8", (0, 1048576), hq=8, hkv=1, d=128, tile=128,
+        sink=128, window=2048, last=128, seed=1007,
+        note="maximum-size check: one 1M-token sequence, 8 query heads on one "
+             "kv head (64-bit addressing, Last rows split 456 ways)"),
     "llama8b_probe_n2048": Workload(
         "llama8b_probe_n2048", (0, 2048), hq=32, hkv=8, d=128, tile=128,
         sink=64, window=128, last=128, seed=1006,

@@ -80,3 +80,9 @@ def test_llama_128k_paper_shape():
 def test_llama_32k_streaming_only():
     # L = 0: the Streaming pattern alone (no Last pass, no merge)
     _check_workload("llama8b_n32k", kinds=("triangle",), shape=(128, 2048, 0))
+
+
+def test_triangle_1m_tokens():
+    # the largest case here: one 1M-token sequence (element offsets of Q and
+    # O beyond 2^31 bytes, 8192 k-tiles in a Last q-tile cut into 456 splits)
+    _check_workload("triangle_n1m_g8", kinds=("triangle",), n_random=48)
