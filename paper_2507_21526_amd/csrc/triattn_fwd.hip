@@ -41,6 +41,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kStep = 64;  // keys per inner step
+constexpr int kKeyTable = 2048;  // LDS table of a list item's step keys
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -324,8 +325,23 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     }
     const int na = list_mode ? ka1 * tps : a_hi - a_lo;
     int nsteps = list_mode ? na : na + (b_hi - b_lo);
+    // A list item's step keys are read from the list once, into an LDS
+    // table, so that no step waits on a global load (a global load's wait
+    // would also wait for the K/V copies in flight).  Longer lists than the
+    // table read the list at every step.
+    __shared__ int32_t keytab[kKeyTable];
+    const bool use_tab = list_mode && na <= kKeyTable;
+    if (use_tab) {
+        for (int s = threadIdx.x; s < na; s += NW * 64) {
+            const int kt = min(max(tile_list[s / tps], 0), max_ktile);
+            keytab[s] = kt * a.tile + (s % tps) * kStep;
+        }
+        __syncthreads();
+    }
     auto step_key0 = [&](int s) -> int {
         if (list_mode) {
+            if (use_tab)
+                return keytab[s];
             const int kt = min(max(tile_list[s / tps], 0), max_ktile);
             return kt * a.tile + (s % tps) * kStep;
         }
