@@ -42,12 +42,27 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def code_text(text: str) -> str:
+    """C++ source without comments, blank lines and trailing spaces: what the
+    compiler sees, so that editing a comment keeps the hash."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.rstrip() for line in text.split("\n") if line.strip())
+
+
+def kernel_source_hash(texts=None) -> str:
+    """Hash of the tile kernel's code (comments excluded); `texts` replaces
+    the files' current contents."""
     h = hashlib.sha256()
-    for rel in ("paper_2507_21526_amd/csrc/triattn_fwd.hip",
-                "paper_2507_21526_amd/csrc/triattn_internal.h"):
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+    rels = ("paper_2507_21526_amd/csrc/triattn_fwd.hip",
+            "paper_2507_21526_amd/csrc/triattn_internal.h")
+    for i, rel in enumerate(rels):
+        if texts is not None:
+            text = texts[i]
+        else:
+            with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+                text = f.read()
+        h.update(code_text(text).encode())
     return h.hexdigest()[:16]
 
 

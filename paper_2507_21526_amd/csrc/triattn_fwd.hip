@@ -20,6 +20,11 @@
 //   (bits 2 and 3 of the row index swapped) so that the score registers are
 //   directly the B operand of O^T += V^T P^T, with V staged transposed in
 //   LDS.  Softmax runs in the log2 domain with fp32 state.
+//
+// Q enters and bf16 O leaves through LDS in whole rows (the MFMA register
+// layout would touch 32 rows per load or store instruction); each workgroup
+// trims its key runs to the steps its own rows can reach; a block-sparse
+// list item reads its step keys from the list once, into an LDS table.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
