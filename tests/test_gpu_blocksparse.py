@@ -149,3 +149,21 @@ def test_blocksparse_128k_bench_config():
                                      [0, 127, 128, 65535, 65536, cu[-1] - 1]]))
     _compare(q, k, v, cu, tile, ptr, idx, o, lse, toks,
              f"blocksparse 128K, {len(merges)} split q-tiles")
+
+
+def test_list_longer_than_the_key_table():
+    # one q-tile lists 2050 k-tiles (T = 64, one item, no split): more steps
+    # than the kernel's LDS key table holds, so that item reads its list in
+    # global memory at every step; the other q-tiles list their diagonal
+    cu, tile = [0, 2049 * 64 + 5], 64
+    nq = -(-cu[-1] // tile)
+    ptr, idx = [0], []
+    for t in range(nq):
+        idx.extend(range(t + 1) if t == nq - 1 else [t])
+        ptr.append(len(idx))
+    log(f"case blocksparse long list: {nq} q-tiles, last lists {nq} tiles")
+    q, k, v = draw_qkv(cu, 2, 1, 64, 91)
+    o, lse, plan = _run_bs(q.cuda(), k.cuda(), v.cuda(), cu, tile, ptr, idx, 100000)
+    assert plan.info.n_merge_items == 0
+    toks = np.concatenate([np.arange((nq - 1) * tile, cu[-1]), [0, 63, 64, 100000]])
+    _compare(q, k, v, cu, tile, ptr, idx, o, lse, toks, "blocksparse long list")
