@@ -323,7 +323,7 @@ def kept_flops(info, hq, tile, d):
 
 def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch,
                    only=None):
-    """Timing of the other workloads: the varlen batch (per-sequence
+    """Timing of the other workloads: the 32K Llama layer, the varlen batch (per-sequence
     schedules), the 28-layer Qwen stack (mixed vs all-dense), block-sparse
     causal attention on the 128K Llama layer, that layer at the paper's own
     Streaming shape (S = 8, W = 512), and the region-contribution probe on a
@@ -336,6 +336,28 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
 
     def want(name):
         return only is None or name in only
+
+    if want("n32k"):
+        # the Llama layer at 32K tokens (per-head scales do not change timing)
+        w = WORKLOADS["llama8b_n32k"]
+        cu = list(w.cu_seqlens)
+        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        o = torch.empty_like(q)
+        tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        t_tri = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 20, 3, torch)
+        t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 5, 1, torch)
+        out["n32k"] = {
+            "workload": w.name, "cu_seqlens": cu,
+            "triangle_ms": t_tri, "dense_ms": t_den,
+            "triangle_kept_tile_tflops": kept_flops(tri.info, w.hq, w.tile, w.d) / t_tri / 1e9,
+            "dense_kept_tile_tflops": kept_flops(den.info, w.hq, w.tile, w.d) / t_den / 1e9,
+            "speedup_vs_dense": t_den / t_tri,
+            "ideal_kept_tile_ratio": den.info.kept_tiles_per_qhead / tri.info.kept_tiles_per_qhead,
+        }
+        del q, k, v, o, tri, den
 
     if want("varlen"):
         # variable-length packed batch
@@ -499,8 +521,8 @@ def main():
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the varlen, 28-layer stack, block-sparse, paper-shape "
                          "and probe timings")
-    ap.add_argument("--section", choices=["varlen", "stack", "blocksparse", "paper_shape",
-                                          "region_probe"],
+    ap.add_argument("--section", choices=["n32k", "varlen", "stack", "blocksparse",
+                                          "paper_shape", "region_probe"],
                     help="run only this one of the other-workload timings (no headline "
                          "step) and print its record; for profiling one kernel")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
