@@ -308,6 +308,32 @@ def ta_region_grad_mean(region_sums, counts) -> np.ndarray:
     return out
 
 
+def region_grad(q, k, v, dout, cu_seqlens, sink, window, last, tile=128,
+                softmax_scale=None, stream=None):
+    """Grad(M-hat, l) of one layer for the (streaming, middle, last)
+    sections, and the per-head sums behind it: the causal pass writes each
+    row's LSE, the probe sums A_ij <dO_i, V_j> per head and section, and the
+    library divides by Hq times the section's pair count.  Returns (grad [3],
+    sums [Hq, 3]) as numpy float64; synchronises the stream to read them."""
+    import torch
+    total, hq, d = q.shape
+    if softmax_scale is None:
+        softmax_scale = 1.0 / float(d) ** 0.5
+    plan = Plan("causal", cu_seqlens, 0, 1, 0, tile, hq, d, device=q.device)
+    o = torch.empty(q.shape, dtype=torch.bfloat16, device=q.device)
+    lse = torch.empty((hq, total), dtype=torch.float32, device=q.device)
+    plan.run(q, k, v, o, lse, softmax_scale, stream)
+    nbytes = ta_probe_workspace_bytes(plan.info, hq)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=q.device) if nbytes else None
+    sums = torch.empty((hq, 3), dtype=torch.float64, device=q.device)
+    region_grad_probe(q, k, v, dout, lse, plan.sched, plan.info, softmax_scale, sink,
+                      window, last, sums, ws, stream)
+    (stream or torch.cuda.current_stream()).synchronize()
+    sums_host = sums.cpu().numpy()
+    return ta_region_grad_mean(sums_host, ta_region_counts(cu_seqlens, sink, window, last)), \
+        sums_host
+
+
 def ta_select_triangle_layers(grad_middle, n_triangle) -> list:
     """The n_triangle layers with the smallest |Grad(middle)|, ascending."""
     g = np.ascontiguousarray(np.asarray(grad_middle, dtype=np.float64))

@@ -121,3 +121,26 @@ def test_probe_total_equals_dout_dot_output_32k():
     err = np.abs(sums.sum(axis=1) - want)
     log(f"  worst |err| / sum|<dO, O>| = {float((err / scale_ref).max()):.2e}")
     assert np.all(err <= 2e-3 * scale_ref)
+
+
+def test_region_grad_helper_matches_oracle_means():
+    # the one-call helper (causal pass for the LSE, probe, counts, means)
+    # against the oracle's sums over its own fp64 causal LSE
+    cu, hq, hkv, d, S, W, L = [0, 600, 1500], 8, 2, 128, 32, 256, 100
+    log("case probe helper")
+    q, k, v = draw_qkv(cu, hq, hkv, d, 51)
+    dout = draw_dout(cu, hq, d, 52)
+    scale = 1.0 / math.sqrt(d)
+    grad, sums = B.region_grad(q.cuda(), k.cuda(), v.cuda(), dout.cuda(), cu, S, W, L,
+                               tile=128)
+    _, lse64 = oracle.attn_full(q, k, v, cu, "causal", 0, 1, 0, scale)
+    want, absw = oracle.region_grad(q, k, v, dout, lse64, cu, S, W, L, scale)
+    # the GPU LSE differs from the fp64 one by ~1e-6 (fp32), which moves
+    # every A_ij by that relative amount
+    assert np.all(np.abs(sums - want) <= 1e-4 * absw + 1e-12)
+    counts = oracle.region_counts(cu, S, W, L)
+    want_grad = want.sum(axis=0) / (hq * counts)
+    assert np.allclose(grad, want_grad, rtol=0,
+                       atol=1e-4 * float(absw.sum(axis=0).max()) / (hq * counts.min()))
+    layers = B.ta_select_triangle_layers([grad[1], 10 * grad[1], 0.1 * grad[1]], 2)
+    assert layers == [0, 2]
