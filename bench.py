@@ -541,7 +541,7 @@ def main():
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only: the "
                           "Triangle attention pass is measured on a single "
-                          "MI355X; multi-GPU runs are not part of this build",
+                          "MI355X; multi-GPU runs are not supported",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 

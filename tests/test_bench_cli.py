@@ -1,6 +1,6 @@
 """The benchmark's command-line contract on the CPU: more than one GPU is
-refused with a message (this build measures one GPU), and the traffic record
-is keyed to the tile kernel's code, not its comments."""
+refused with a message (the benchmark measures one GPU), and the traffic
+record is keyed to the tile kernel's code, not its comments."""
 import json
 import os
 import subprocess
