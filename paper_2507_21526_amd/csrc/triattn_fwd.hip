@@ -45,6 +45,10 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Lambdas of the tile kernel are always inlined: the step loops call several
+// of them more than once and must not turn them into calls.
+#define TA_INLINE __attribute__((always_inline))
+
 constexpr int kStep = 64;  // keys per inner step
 constexpr int kKeyTable = 2048;  // LDS table of a list item's step keys
 constexpr float kLog2e = 1.4426950408889634f;
@@ -131,6 +135,7 @@ __device__ __forceinline__ float pair_sum(float x)
 // when a row maximum grows by more than this many powers of two, so
 // probabilities stay below 2^kRescaleLog2 relative to the stale maximum.
 constexpr float kRescaleLog2 = 8.0f;
+constexpr float kRescaleBound = 256.0f;  // 2^kRescaleLog2
 
 // Register fences: an empty volatile asm that reads and rewrites a value, so
 // the computation producing it cannot be moved past this point (side-effect
@@ -152,19 +157,17 @@ __device__ __forceinline__ void fence_regs(float &x)
 // (lane l lands at lds_addr + 16 l).  Issued from inline assembly so that the
 // compiler does not serialise it against unrelated LDS reads (the copy
 // targets the other LDS stage; barriers order it against the readers of its
-// own stage): completion is tracked explicitly with vmcnt waits.  M0 holds
-// the LDS address during the copy and is restored afterwards.
+// own stage): completion is tracked explicitly with vmcnt waits.  The LDS
+// address is bound to M0 through the operand constraint, so the compiler
+// writes M0 itself (one scalar add per copy) and knows its value; the nop
+// is the wait state between that write and the copy reading it.
 __device__ __forceinline__ void copy_to_lds16(const void *gbase, uint32_t lane_byte_off,
                                               uint32_t lds_addr)
 {
-    uint32_t saved;
-    asm volatile("s_mov_b32 %0, m0\n\t"
-                 "s_mov_b32 m0, %1\n\t"
-                 "s_nop 0\n\t"
-                 "global_load_lds_dwordx4 %2, %3\n\t"
-                 "s_mov_b32 m0, %0"
-                 : "=&s"(saved)
-                 : "s"(lds_addr), "v"(lane_byte_off), "s"(gbase));
+    asm volatile("s_nop 0\n\t"
+                 "global_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(lane_byte_off), "s"(gbase), "{m0}"(lds_addr));
 }
 
 // Workgroup barrier without a memory fence: this wave's LDS reads are
@@ -343,7 +346,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         }
         __syncthreads();
     }
-    auto step_key0 = [&](int s) -> int {
+    auto step_key0 = [&](int s) TA_INLINE -> int {
         if (list_mode) {
             if (use_tab)
                 return keytab[s];
@@ -378,7 +381,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         }
     }
     bf16x8 qf[QK_STEPS];
-    auto read_q = [&]() {
+    auto read_q = [&]() TA_INLINE {
         const unsigned char *qt = smem + QREGION + wave * QTILE_BYTES + col * ROW_BYTES;
 #pragma unroll
         for (int s = 0; s < QK_STEPS; ++s)
@@ -398,58 +401,77 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const int dma_row_in = lane / CHUNKS;
     const int dma_pc = lane % CHUNKS;
     // The swizzle of row m * ROWS_PER_DMA + i is swizzle(i) ^ swizzle of the
-    // copy's first row (K) or swizzle(i) (V), so two per-lane constants give
-    // the stored chunk of every copy.
+    // copy's first row (K) or swizzle(i) (V): the copy's first row is a
+    // multiple of ROWS_PER_DMA, whose swizzle bits lie above those of i.
     const uint32_t kx0 = (uint32_t)((dma_pc ^ kswz<D>(dma_row_in)) << 4);
     const uint32_t vx0 = (uint32_t)((dma_pc ^ vswz<D>(dma_row_in)) << 4);
     const uint32_t row_stride_bytes = 2u * (uint32_t)tok_stride;  // < 2^24 (host check)
+    // Byte offset of the row of the tile that this lane copies in the wave's
+    // first copy, and the step from one of the wave's copies to the next.
+    const uint32_t dma_off0 =
+        __umul24((uint32_t)(wave * ROWS_PER_DMA + dma_row_in), row_stride_bytes);
+    const uint32_t dma_off_step = (uint32_t)(N_COPY_WAVES * ROWS_PER_DMA) * row_stride_bytes;
+    // The K swizzle term of copy i, kswz((wave + i * N_COPY_WAVES) *
+    // ROWS_PER_DMA), does not depend on i when N_COPY_WAVES * ROWS_PER_DMA
+    // is a multiple of the swizzle period (16 rows for d = 128, 8 rows of
+    // bit 1..3 for d = 64): then one clamp bound per tile serves every copy.
+    constexpr bool XR_PER_WAVE = D == 128 ? N_COPY_WAVES % 4 == 0 : N_COPY_WAVES % 2 == 0;
     // Keys past the end of the sequence are read from its last row: they lie
     // beyond every row of the item, so the causal mask gives them p = 0.
     const int key_max = seq_len - 1;
 
     // One tile copy (K or V of one step into one stage).  Row r of the tile
     // reads key min(key0 + r, last key of the sequence), so a step past the
-    // end of the sequence still reads valid rows.  Copy m starts from the
-    // scalar base key b = min(key0 + m * ROWS_PER_DMA, last key) and lane
-    // row i adds min(i, last key - b) rows: an unsigned 32-bit byte offset
-    // that is never negative.
+    // end of the sequence still reads valid rows.  The scalar base is the
+    // tile's first key kc = min(key0, last key); lane row r adds the byte
+    // offset min(r, last key - kc) * row pitch (the clamp is taken on the
+    // byte offsets, which are monotonic in r), an unsigned 32-bit offset of
+    // fewer than 64 rows that is never negative.  Everything that depends
+    // only on the tile is computed once here, so a copy costs one M0 write,
+    // a nop, three vector instructions and the copy itself.
     struct TileCopy {
-        const uint16_t *src;
-        uint32_t lds;
-        int key0;
+        const uint16_t *base;  // row kc of the source
+        uint32_t lds;          // LDS address of this wave's first copy
+        uint32_t lim;          // min(last key - kc, 63) * row pitch in bytes
     };
-    auto plan_copy = [&](const uint16_t *src, int key0, int buf, bool is_v) -> TileCopy {
+    auto plan_copy = [&](const uint16_t *src, int key0, int buf,
+                         bool is_v) TA_INLINE -> TileCopy {
+        // key0 is the same on every lane (it may come from the LDS key table)
+        const int kc = __builtin_amdgcn_readfirstlane(min(key0, key_max));
         TileCopy t;
-        t.src = src;
-        t.key0 = key0;
-        t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0);
+        t.base = src + (int64_t)kc * tok_stride;
+        t.lim = (uint32_t)min(key_max - kc, kStep - 1) * row_stride_bytes;
+        t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0) + wave * 1024;
         return t;
     };
     // Copy i of this wave (m = wave + i * N_COPY_WAVES) of a planned tile.
-    auto issue_copy = [&](const TileCopy &t, int i, bool is_v) {
+    auto issue_copy = [&](const TileCopy &t, int i, bool is_v) TA_INLINE {
         const int m = wave + i * N_COPY_WAVES;
         if constexpr (N_DMA % N_COPY_WAVES != 0) {
             if (m >= N_DMA)
                 return;
         }
-        const int sc = m * ROWS_PER_DMA;
-        const int base_key = min(t.key0 + sc, key_max);
-        const int lim = key_max - base_key;
-        const uint16_t *base = t.src + (int64_t)base_key * tok_stride;
-        const uint32_t xr = is_v ? vx0 : (kx0 ^ (uint32_t)(kswz<D>(sc) << 4));
-        const uint32_t off = __umul24((uint32_t)min(dma_row_in, lim), row_stride_bytes) + xr;
-        copy_to_lds16(base, off, t.lds + m * 1024);
+        const uint32_t xr = is_v ? vx0 : (kx0 ^ (uint32_t)(kswz<D>(m * ROWS_PER_DMA) << 4));
+        uint32_t off;
+        if constexpr (XR_PER_WAVE) {
+            // min(r, lim) + xr = min(r + xr, lim + xr): the first term is a
+            // constant of the lane and copy, the second of the lane and tile
+            off = min(dma_off0 + (uint32_t)i * dma_off_step + xr, t.lim + xr);
+        } else {
+            off = min(dma_off0 + (uint32_t)i * dma_off_step, t.lim) + xr;
+        }
+        copy_to_lds16(t.base, off, t.lds + i * (N_COPY_WAVES * 1024));
     };
     // Copy slot c (0 <= c < 2 * COPIES): K copies first, then V copies.
     TileCopy cp_k{}, cp_v{};
-    auto issue_slot = [&](int c) {
+    auto issue_slot = [&](int c) TA_INLINE {
         if (c < COPIES)
             issue_copy(cp_k, c, false);
         else
             issue_copy(cp_v, c - COPIES, true);
     };
     // Hook run after MFMA number `slot` of a matrix phase of a copy wave.
-    auto copy_hook = [&](int slot) {
+    auto copy_hook = [&](int slot) TA_INLINE {
         if (slot % COPY_STRIDE == COPY_STRIDE - 1 && slot / COPY_STRIDE < 2 * COPIES)
             issue_slot(slot / COPY_STRIDE);
     };
@@ -464,7 +486,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
 #pragma unroll
     for (int s = 0; s < QK_STEPS; ++s)
         koff[s] = (uint32_t)(krow0 * ROW_BYTES + (((2 * s + half) ^ kswz<D>(krow0)) << 4));
-    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) {
+    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) TA_INLINE {
         const unsigned char *kt = smem + buf * STAGE_BYTES;
         sacc[0] = f32x16{};
         sacc[1] = f32x16{};
@@ -510,7 +532,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         voff[b] = (uint32_t)(vrow0 * ROW_BYTES + (((d >> 3) ^ vswz<D>(vrow0)) << 4) +
                              (d & 7) * 2);
     }
-    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) {
+    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) TA_INLINE {
         const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -544,7 +566,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
 
     // Element mask (branch-free selects) where the step crosses the diagonal
     // or the window edge; keys beyond the sequence are beyond every row.
-    auto mask_step = [&](int key0, f32x16 (&sacc)[2]) {
+    auto mask_step = [&](int key0, f32x16 (&sacc)[2]) TA_INLINE {
         const int lim = my_row - key0 - 8 * half;        // key offset <= lim
         // streaming rows also need offset < sink_lim or offset > win_lim
         const bool stream_mode = mode == kModeStreaming;
@@ -559,7 +581,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
                 sacc[kb][v] = keep ? sacc[kb][v] : -INFINITY;
             }
     };
-    auto step_needs_mask = [&](int key0) -> bool {
+    auto step_needs_mask = [&](int key0) TA_INLINE -> bool {
         return (key0 + kStep - 1 > row_base) ||
                (mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
                 row_hi - key0 >= a.window);
@@ -571,40 +593,51 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     // Online softmax of one step: probabilities relative to the (lazily
     // re-based) reference maximum, converted to the bf16 B operand of PV.
     // O holds every earlier step already, so a re-base rescales it here.
-    auto softmax = [&](f32x16 (&sacc)[2], bf16x8 (&pf)[2][2]) {
-        float mx = -INFINITY;
+    // The probabilities are first taken against the current reference: each
+    // is >= 0, so if their sum is at most 2^kRescaleLog2 none exceeds it and
+    // the step needs no row maximum at all.  Only when the sum is larger (a
+    // maximum grew by about that much) or the reference is not set yet does
+    // the wave compute the row maxima, re-base and redo the step; the result
+    // is the same lazy re-base as comparing each new maximum with the
+    // reference, without the maximum's instructions on ordinary steps.
+    auto softmax = [&](f32x16 (&sacc)[2], bf16x8 (&pf)[2][2]) TA_INLINE {
+        auto exp_step = [&](float m_use) TA_INLINE -> float {
+            float psum = 0.f;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v)
-                mx = fmaxf(mx, sacc[kb][v]);
-        mx = pair_max(mx);
-        const float m_new = fmaxf(m_ref, mx * c);
-        const bool need = __builtin_amdgcn_ballot_w64(m_new > m_ref + kRescaleLog2) != 0;
-        const float m_upd = need ? m_new : m_ref;
-        const float m_use = (m_upd == -INFINITY) ? 0.f : m_upd;
-        if (need) {
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    f32x8 t;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        t[e] = __builtin_amdgcn_exp2f(
+                            __builtin_fmaf(sacc[kb][8 * s2 + e], c, -m_use));
+                        psum += t[e];
+                    }
+                    pf[kb][s2] = __builtin_convertvector(t, bf16x8);
+                }
+            return psum;
+        };
+        float psum = exp_step(m_ref == -INFINITY ? 0.f : m_ref);
+        const bool bad = !(psum <= kRescaleBound) || m_ref == -INFINITY;
+        if (__builtin_amdgcn_ballot_w64(bad) != 0) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    mx = fmaxf(mx, sacc[kb][v]);
+            mx = pair_max(mx);
+            const float m_new = fmaxf(m_ref, mx * c);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
             const float alpha = __builtin_amdgcn_exp2f(m_ref - m_use);
             l_run *= alpha;
 #pragma unroll
             for (int b = 0; b < D_BLOCKS; ++b)
                 oacc[b] *= alpha;
+            m_ref = m_new;
+            psum = exp_step(m_use);
         }
-        m_ref = m_upd;
-        float psum = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int s2 = 0; s2 < 2; ++s2) {
-                f32x8 t;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    t[e] = __builtin_amdgcn_exp2f(
-                        __builtin_fmaf(sacc[kb][8 * s2 + e], c, -m_use));
-                    psum += t[e];
-                }
-                pf[kb][s2] = __builtin_convertvector(t, bf16x8);
-            }
         l_run += psum;
     };
 
@@ -626,11 +659,14 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     bf16x8 p_acc[2][2];
 
     // Matrix phase: QK^T of step j (if any) and PV of step j-1 (if any).
-    auto do_m = [&](int j, bool has_qk, bool has_pv, auto hook) {
+    // Inside the step loops (unrolled by two) the LDS stage is a
+    // std::integral_constant, so every LDS operand address is a per-lane
+    // offset plus an immediate.
+    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(1);  // MFMA issue goes first on the SIMD
         __builtin_amdgcn_sched_barrier(0);
-        const int buf = j & 1;
+        const int buf = stage;
         if (has_qk)
             qk(buf, s_acc, hook);
         if (has_pv)
@@ -639,7 +675,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         __builtin_amdgcn_s_setprio(0);
         __builtin_amdgcn_sched_barrier(0);
     };
-    auto do_x = [&](int j) {
+    auto do_x = [&](int j) TA_INLINE {
         const int key0 = step_key0(j);
         if (step_needs_mask(key0))
             mask_step(key0, s_acc);
@@ -654,7 +690,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     };
     // A phase boundary: the scheduler may not move any instruction across it
     // (MFMAs and VALU work must stay in their own phase).
-    auto end_phase = [&](bool wait_copies) {
+    auto end_phase = [&](bool wait_copies) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
         if (wait_copies)
             wait_vmcnt(0);
@@ -663,10 +699,13 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     };
     // Copies of K(j+1) and V(j) into stage (j+1) & 1 (clamped sources: copies
     // for steps past the last one land in parts of the stage nobody reads).
-    auto plan_step_copies = [&](int j) {
-        cp_k = plan_copy(kbase, step_key0(min(j + 1, nsteps - 1)), (j + 1) & 1, false);
-        cp_v = plan_copy(vbase, step_key0(min(j, nsteps - 1)), (j + 1) & 1, true);
+    auto plan_step_copies = [&](int j, auto stage) TA_INLINE {
+        const int nbuf = 1 - (int)stage;  // stage (j + 1) & 1
+        cp_k = plan_copy(kbase, step_key0(min(j + 1, nsteps - 1)), nbuf, false);
+        cp_v = plan_copy(vbase, step_key0(min(j, nsteps - 1)), nbuf, true);
     };
+    using Stage0 = std::integral_constant<int, 0>;
+    using Stage1 = std::integral_constant<int, 1>;
 
     if (nsteps > 0) {
         // Prologue: the copy waves copy K(0) into stage 0.
@@ -680,8 +719,8 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         read_q();
         if (group == 0) {
             // j = 0: QK only, then the copies of the PV slots.
-            plan_step_copies(0);
-            do_m(0, true, false, copy_hook);
+            plan_step_copies(0, Stage0{});
+            do_m(Stage0{}, true, false, copy_hook);
 #pragma unroll
             for (int c = 0; c < 2 * COPIES; ++c)
                 if (c * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
@@ -689,29 +728,44 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
             end_phase(false);
             do_x(0);
             end_phase(true);
-            for (int j = 1; j < nsteps; ++j) {
-                plan_step_copies(j);
-                do_m(j, true, true, copy_hook);
+            // step j reads stage j & 1 (odd j first)
+            auto step = [&](int j, auto stage) TA_INLINE {
+                plan_step_copies(j, stage);
+                do_m(stage, true, true, copy_hook);
                 end_phase(false);
                 do_x(j);
                 end_phase(true);
+            };
+            int j = 1;
+            for (; j + 1 < nsteps; j += 2) {
+                step(j, Stage1{});
+                step(j + 1, Stage0{});
             }
-            do_m(nsteps, false, true, no_hook);
+            if (j < nsteps)
+                step(j, Stage1{});
+            do_m(nsteps & 1, false, true, no_hook);
             end_phase(false);
             end_phase(false);
         } else {
             end_phase(false);
-            do_m(0, true, false, no_hook);
+            do_m(Stage0{}, true, false, no_hook);
             end_phase(false);
-            for (int j = 1; j < nsteps; ++j) {
+            auto step = [&](int j, auto stage) TA_INLINE {
                 do_x(j - 1);
                 end_phase(false);
-                do_m(j, true, true, no_hook);
+                do_m(stage, true, true, no_hook);
                 end_phase(false);
+            };
+            int j = 1;
+            for (; j + 1 < nsteps; j += 2) {
+                step(j, Stage1{});
+                step(j + 1, Stage0{});
             }
+            if (j < nsteps)
+                step(j, Stage1{});
             do_x(nsteps - 1);
             end_phase(false);
-            do_m(nsteps, false, true, no_hook);
+            do_m(nsteps & 1, false, true, no_hook);
             end_phase(false);
         }
     } else {
