@@ -1,0 +1,79 @@
+"""GPU parity of the online softmax's re-base paths against the fp64 oracle.
+
+The tile kernel re-bases a row's reference maximum lazily: a step's
+probabilities are first taken against the current reference, and the wave
+computes the row maxima, rescales O and l and redoes the step only when the
+step's probability sum exceeds 2^8 (or no reference is set yet).  Standard
+normal inputs at scale 1/sqrt(d) almost never take that path after the
+first step, so these inputs force it: keys whose scores grow along the
+sequence (many re-bases per row), a softmax scale of 1 (scores spread over
+tens of powers of two), and isolated keys with huge scores (one large jump,
+after which every other probability underflows).  Each output row is the
+softmax of Sec. 2.1 over the kept keys, compared with the oracle on every
+row and head.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2507_21526_amd.inputs import draw_qkv
+from tests.parity import bf16_p_bound, compare, log, run_pass
+
+pytestmark = pytest.mark.gpu
+
+CU = [0, 1500, 2900]
+HQ, HKV, D = 8, 2, 128
+S, W, L, T = 64, 512, 200, 128
+
+
+def _bf16(x):
+    return x.float().to(torch.bfloat16)
+
+
+def _check(kind, q, k, v, scale, label):
+    qg, kg, vg = (t.to("cuda:0") for t in (q, k, v))
+    o, lse, _ = run_pass(kind, qg, kg, vg, CU, S, W, L, T, 0, scale=scale,
+                         poison=True)
+    torch.cuda.synchronize()
+    assert not torch.isnan(o).any(), f"{label}: unwritten or NaN output rows"
+    compare(kind, q, k, v, CU, S, W, L, scale, o, lse, np.arange(CU[-1]),
+            range(HQ), label=label, max_abs=bf16_p_bound(v))
+
+
+@pytest.mark.parametrize("kind", ["triangle", "causal"])
+def test_rebase_growing_keys(kind):
+    # key j of a sequence of n tokens scaled by 1 + 4 j / n: the row maximum
+    # keeps growing along the keys, by about 20 powers of two overall
+    log(f"case rebase growing keys {kind}")
+    q, k, v = draw_qkv(CU, HQ, HKV, D, seed=41)
+    f = torch.ones(CU[-1])
+    for b in range(len(CU) - 1):
+        n = CU[b + 1] - CU[b]
+        f[CU[b]:CU[b + 1]] = 1.0 + 4.0 * torch.arange(n) / n
+    k = _bf16(k.float() * f.view(-1, 1, 1))
+    _check(kind, q, k, v, D ** -0.5, f"rebase growing keys {kind}")
+
+
+@pytest.mark.parametrize("kind", ["triangle", "causal"])
+def test_rebase_unit_scale(kind):
+    # softmax scale 1 instead of 1/sqrt(d): scores of standard deviation
+    # about 11, so step sums leave the 2^8 bound often
+    log(f"case rebase unit scale {kind}")
+    q, k, v = draw_qkv(CU, HQ, HKV, D, seed=42)
+    _check(kind, q, k, v, 1.0, f"rebase unit scale {kind}")
+
+
+@pytest.mark.parametrize("kind", ["triangle", "causal"])
+def test_rebase_spikes(kind):
+    # a few keys per sequence (in the sink, the band and the middle) with
+    # 30x the norm: rows that see one jump by far more than 2^8
+    log(f"case rebase spikes {kind}")
+    q, k, v = draw_qkv(CU, HQ, HKV, D, seed=43)
+    k = k.float()
+    for b in range(len(CU) - 1):
+        for r in (3, 700, 1100, 1400):
+            j = CU[b] + r
+            if j < CU[b + 1]:
+                k[j] *= 30.0
+    k = _bf16(k)
+    _check(kind, q, k, v, D ** -0.5, f"rebase spikes {kind}")
