@@ -326,8 +326,9 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
     """Timing of the other workloads: the 32K Llama layer, the varlen batch (per-sequence
     schedules), the 28-layer Qwen stack (mixed vs all-dense), block-sparse
     causal attention on the 128K Llama layer, that layer at the paper's own
-    Streaming shape (S = 8, W = 512), and the region-contribution probe on a
-    Llama layer at 2K and 32K tokens."""
+    Streaming shape (S = 8, W = 512), a multi-head (group 1) layer at 32K
+    tokens, and the region-contribution probe on a Llama layer at 2K and 32K
+    tokens."""
     import numpy as np
 
     from paper_2507_21526_amd.inputs import blocksparse_lists
@@ -464,6 +465,27 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         }
         del q, k, v, o, ps
 
+    if want("mha"):
+        # multi-head attention (group 1): four-wave workgroups, two per CU
+        w = WORKLOADS["mha_n32k"]
+        cu = list(w.cu_seqlens)
+        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        o = torch.empty_like(q)
+        tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
+                           device=dev)
+        t_tri = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 20, 3, torch)
+        t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 5, 1, torch)
+        out["mha"] = {
+            "workload": w.name, "cu_seqlens": cu, "hq": w.hq, "hkv": w.hkv,
+            "triangle_ms": t_tri, "dense_ms": t_den,
+            "triangle_kept_tile_tflops": kept_flops(tri.info, w.hq, w.tile, w.d) / t_tri / 1e9,
+            "dense_kept_tile_tflops": kept_flops(den.info, w.hq, w.tile, w.d) / t_den / 1e9,
+            "speedup_vs_dense": t_den / t_tri,
+        }
+        del q, k, v, o, tri, den
+
     if want("region_probe"):
         # region-contribution probe (Sec. 2.2): one Llama-3.1-8B layer with the
         # probe's sections (si 64, sl 128, last 128) on the paper's ~2K-token
@@ -519,10 +541,10 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
-                    help="skip the varlen, 28-layer stack, block-sparse, paper-shape "
-                         "and probe timings")
+                    help="skip the 32K, varlen, 28-layer stack, block-sparse, "
+                         "paper-shape, multi-head and probe timings")
     ap.add_argument("--section", choices=["n32k", "varlen", "stack", "blocksparse",
-                                          "paper_shape", "region_probe"],
+                                          "paper_shape", "mha", "region_probe"],
                     help="run only this one of the other-workload timings (no headline "
                          "step) and print its record; for profiling one kernel")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)

@@ -132,18 +132,13 @@ __device__ __forceinline__ float pair_sum(float x)
 }
 
 // Running maxima are re-based lazily: the output accumulator is rescaled only
-// when a row maximum grows by more than this many powers of two, so
-// probabilities stay below 2^kRescaleLog2 relative to the stale maximum.
-constexpr float kRescaleLog2 = 8.0f;
-constexpr float kRescaleBound = 256.0f;  // 2^kRescaleLog2
+// when a step's probabilities against the stale maximum could exceed this
+// bound (2^8), so every probability stays at most 2^8.
+constexpr float kRescaleBound = 256.0f;
 
 // Register fences: an empty volatile asm that reads and rewrites a value, so
 // the computation producing it cannot be moved past this point (side-effect
 // free arithmetic could otherwise be sunk across a phase boundary).
-__device__ __forceinline__ void fence_regs(f32x16 &x)
-{
-    asm volatile("" : "+v"(x));
-}
 __device__ __forceinline__ void fence_regs(bf16x8 &x)
 {
     asm volatile("" : "+v"(x));
@@ -222,7 +217,8 @@ __device__ __forceinline__ int vswz(int r)
 }
 
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t kind)
+__global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(FwdArgs a,
+                                                                               int32_t kind)
 {
     constexpr int ROW_BYTES = 2 * D;
     constexpr int CHUNKS = D / 8;                       // 16-byte chunks per row
@@ -242,11 +238,18 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
                                     ? MFMA_SLOTS / (2 * COPIES) : 1;
 
     // LDS: the two K/V stages, then one 32-row Q tile per wave (the prologue
-    // stages Q there so that it is read from HBM in whole rows).
+    // stages Q there so that it is read from HBM in whole rows).  Workgroups
+    // of at most four waves put their Q tiles in stage 1 instead, which
+    // receives its first K/V copies only after every wave has read them:
+    // their LDS then allows two workgroups per CU, and for four waves the
+    // launch bound keeps them within 256 registers, so that every SIMD holds
+    // two waves (the two of one workgroup's ping-pong pair sit on different
+    // SIMDs).
     constexpr int QTILE_BYTES = 32 * ROW_BYTES;
-    constexpr int QREGION = N_STAGES * STAGE_BYTES;
+    constexpr bool Q_IN_STAGE = NW * QTILE_BYTES <= STAGE_BYTES;
+    constexpr int QREGION = Q_IN_STAGE ? STAGE_BYTES : N_STAGES * STAGE_BYTES;
     __shared__ __attribute__((aligned(1024))) unsigned char
-        smem[N_STAGES * STAGE_BYTES + NW * QTILE_BYTES];
+        smem[N_STAGES * STAGE_BYTES + (Q_IN_STAGE ? 0 : NW * QTILE_BYTES)];
 
     const int32_t *sched = a.sched;
     int bid = blockIdx.x;
@@ -303,7 +306,6 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     const bool wave_active = row_base < r1;
     const int my_row = row_base + col;            // sequence-relative row
     const bool row_valid = my_row < r1;
-    const int load_row = row_valid ? my_row : r1 - 1;
     const int row_hi = (r1 - 1 < row_base + 31) ? r1 - 1 : row_base + 31;
     const float c = a.scale_log2;
 
@@ -576,7 +578,7 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int off = kb * 32 + (v & 7) + 16 * (v >> 3);
+                const int off = kb * 32 + key_of_reg(v, 0);  // 8 half is in lim
                 const bool keep = (off <= lim) & ((off < sink_lim) | (off > win_lim));
                 sacc[kb][v] = keep ? sacc[kb][v] : -INFINITY;
             }
@@ -594,12 +596,13 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
     // re-based) reference maximum, converted to the bf16 B operand of PV.
     // O holds every earlier step already, so a re-base rescales it here.
     // The probabilities are first taken against the current reference: each
-    // is >= 0, so if their sum is at most 2^kRescaleLog2 none exceeds it and
+    // is >= 0, so if their sum is at most kRescaleBound none exceeds it and
     // the step needs no row maximum at all.  Only when the sum is larger (a
-    // maximum grew by about that much) or the reference is not set yet does
-    // the wave compute the row maxima, re-base and redo the step; the result
-    // is the same lazy re-base as comparing each new maximum with the
-    // reference, without the maximum's instructions on ordinary steps.
+    // maximum has grown by up to log2(kRescaleBound) powers of two or more)
+    // or no reference is set yet does the wave compute the row maxima,
+    // re-base to them and redo the step.  Either way every probability that
+    // enters O and l is at most kRescaleBound and the row maximum itself,
+    // once seen, contributes at least 1 (no underflow of l).
     auto softmax = [&](f32x16 (&sacc)[2], bf16x8 (&pf)[2][2]) TA_INLINE {
         auto exp_step = [&](float m_use) TA_INLINE -> float {
             float psum = 0.f;
@@ -717,6 +720,8 @@ __global__ __launch_bounds__(NW * 64) void attn_tile_kernel(FwdArgs a, int32_t k
         }
         end_phase(true);  // K(0) and every wave's Q tile have landed
         read_q();
+        if constexpr (Q_IN_STAGE)
+            end_phase(false);  // stage 1 is free once every wave has read its Q
         if (group == 0) {
             // j = 0: QK only, then the copies of the PV slots.
             plan_step_copies(0, Stage0{});

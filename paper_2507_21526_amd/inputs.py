@@ -74,6 +74,11 @@ WORKLOADS = {
         sink=128, window=2048, last=128, seed=1007,
         note="maximum-size check: one 1M-token sequence, 8 query heads on one "
              "kv head (64-bit addressing, Last rows split 456 ways)"),
+    "mha_n32k": Workload(
+        "mha_n32k", (0, 32768), hq=32, hkv=32, d=128, tile=128, sink=128,
+        window=2048, last=128, seed=1008,
+        note="multi-head attention (GQA group 1, the Llama-2-7B attention "
+             "shape), N=32768: four-wave workgroups, two per CU"),
     "llama8b_probe_n2048": Workload(
         "llama8b_probe_n2048", (0, 2048), hq=32, hkv=8, d=128, tile=128,
         sink=64, window=128, last=128, seed=1006,

@@ -71,6 +71,12 @@ def test_qwen_stack_layers():
     _check_workload("qwen7b_n128k_stack28", dense[0], kinds=("causal",))
 
 
+def test_mha_32k():
+    # group 1: four-wave workgroups with their Q tiles in LDS stage 1, two
+    # workgroups per CU
+    _check_workload("mha_n32k")
+
+
 def test_llama_128k_paper_shape():
     # the paper's own Streaming shape (sink 8, window 512; the sink is not
     # tile aligned), timed by the benchmark next to the paper's speedup
