@@ -61,6 +61,7 @@ EDGE = [
     ([0, 1500], 16, 2, 128, 1, 1, 1, 128),         # W = 1, L = 1: 2 keys/row
     ([0, 777], 5, 5, 64, 8, 512, 50, 128),         # MHA, paper's S/W
     ([0, 2000], 6, 3, 128, 64, 128, 128, 64),      # paper probing shape
+    ([0, 1100], 3, 3, 128, 16, 300, 40, 64),       # G = 1, d 128, T 64: two waves
 ]
 
 
