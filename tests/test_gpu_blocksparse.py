@@ -62,6 +62,8 @@ CASES = [
     ([0, 0, 333, 900, 901], 28, 4, 128, 64, 0.6, None, 3),  # varlen, G = 7
     ([0, 1500], 16, 2, 128, 128, 0.1, None, 0),     # sparse, some empty rows
     ([0, 520], 3, 1, 64, 128, 1.0, None, 2),        # full lists cut in splits
+    ([0, 1200], 4, 4, 128, 128, 0.4, None, 0),      # G = 1: Q tiles in a K/V stage
+    ([0, 900], 2, 2, 64, 64, 0.5, True, 1),         # G = 1, T = 64: two waves
 ]
 
 
