@@ -317,6 +317,15 @@ def timed_pass(binding, plan, q, k, v, o, scale, stream, steps, warmup, torch):
     return e0.elapsed_time(e1) / steps
 
 
+def element_exact(binding, cu, w, d, ms):
+    """FLOPs of the kept (row, key) pairs alone: 4 d per pair and query head,
+    pairs per head from the closed-form section counts."""
+    counts = binding.ta_region_counts(cu, w.sink, w.window, w.last)
+    pairs = int(counts[0]) + int(counts[2])  # streaming + last; middle skipped
+    flops = 4.0 * d * w.hq * pairs
+    return {"pairs_per_head": pairs, "flops": flops, "tflops": flops / ms / 1e9}
+
+
 def kept_flops(info, hq, tile, d):
     return float(info.kept_tiles_per_qhead) * hq * 4.0 * tile * tile * d
 
@@ -725,6 +734,9 @@ def main():
         "merge": {"kernel_ms": merge_ms, "algorithmic_bytes": merge_bytes,
                   "gbs": merge_gbs, "frac_of_hbm_peak":
                   (merge_gbs / PEAK_HBM_GBS) if merge_gbs else None},
+        # the same step counted on the (row, key) pairs the Triangle mask keeps
+        # (streaming and Last sections, closed form) instead of whole tiles
+        "element_exact": element_exact(binding, cu, w, d, ms_per_step),
         "dense_causal": dense_rec,
         "speedup_vs_dense": (dense_rec["ms_per_step"] / ms_per_step) if dense_rec else None,
         "other_workloads": extra,
