@@ -71,6 +71,8 @@ def load():
                                      ctypes.c_int, i64, i64, i64, dbl,
                                      vp, vp, i64, vp, vp]
     lib.oracle_attn_rows.restype = ctypes.c_int
+    lib.oracle_attn_rows_absw.argtypes = list(lib.oracle_attn_rows.argtypes) + [vp]
+    lib.oracle_attn_rows_absw.restype = ctypes.c_int
     lib.oracle_schedule.argtypes = [ctypes.c_int, vp, i32, i32, i32, i32, i32,
                                     i32, vp, i64]
     lib.oracle_schedule.restype = i64
@@ -143,11 +145,14 @@ def mask_nnz(kind, n, sink, window, last) -> int:
 
 
 def attn_rows(q, k, v, cu_seqlens, kind, sink, window, last, scale,
-              row_tok, row_head):
+              row_tok, row_head, with_absw=False):
     """fp64 output rows and natural-log LSE for (token, query head) pairs.
 
     q: [total, Hq, d], k/v: [total, Hkv, d] as torch bf16 (or uint16 bits).
-    Returns (out [nrows, d] float64, lse [nrows] float64).
+    Returns (out [nrows, d] float64, lse [nrows] float64), and with
+    ``with_absw`` also absw [nrows, d]: sum_j p_j |v_j| per element (the
+    probability-weighted mean of |v|, which bounds the effect of relative
+    rounding errors in the probabilities on the output).
     """
     qb, kb, vb = _bf16_bits(q), _bf16_bits(k), _bf16_bits(v)
     total, hq, d = qb.shape
@@ -159,14 +164,18 @@ def attn_rows(q, k, v, cu_seqlens, kind, sink, window, last, scale,
     assert rt.shape == rh.shape
     out = np.zeros((rt.size, d), dtype=np.float64)
     lse = np.zeros(rt.size, dtype=np.float64)
-    rc = load().oracle_attn_rows(qb.ctypes.data, kb.ctypes.data, vb.ctypes.data,
-                                 cu.ctypes.data, cu.size - 1, hq, hkv, d,
-                                 _kind(kind), sink, window, last, float(scale),
-                                 rt.ctypes.data, rh.ctypes.data, rt.size,
-                                 out.ctypes.data, lse.ctypes.data)
+    args = (qb.ctypes.data, kb.ctypes.data, vb.ctypes.data, cu.ctypes.data,
+            cu.size - 1, hq, hkv, d, _kind(kind), sink, window, last,
+            float(scale), rt.ctypes.data, rh.ctypes.data, rt.size,
+            out.ctypes.data, lse.ctypes.data)
+    if with_absw:
+        absw = np.zeros((rt.size, d), dtype=np.float64)
+        rc = load().oracle_attn_rows_absw(*args, absw.ctypes.data)
+    else:
+        rc = load().oracle_attn_rows(*args)
     if rc != 0:
         raise ValueError("oracle_attn_rows rejected the request")
-    return out, lse
+    return (out, lse, absw) if with_absw else (out, lse)
 
 
 def attn_full(q, k, v, cu_seqlens, kind, sink, window, last, scale):

@@ -122,7 +122,7 @@ static int attn_rows_core(const uint16_t *q, const uint16_t *k, const uint16_t *
                           int32_t hkv, int32_t d, const mask_src *ms,
                           double scale, const int64_t *row_tok,
                           const int32_t *row_head, int64_t nrows, double *out,
-                          double *lse)
+                          double *lse, double *absw)
 {
     if (batch < 0 || hq <= 0 || hkv <= 0 || d <= 0 || hq % hkv != 0)
         return -1;
@@ -179,8 +179,12 @@ static int attn_rows_core(const uint16_t *q, const uint16_t *k, const uint16_t *
                     zmax = z[j];
             }
             double *o = out + (size_t)r * d;
+            double *aw = absw ? absw + (size_t)r * d : NULL;
             for (int32_t c = 0; c < d; ++c)
                 o[c] = 0.0;
+            if (aw)
+                for (int32_t c = 0; c < d; ++c)
+                    aw[c] = 0.0;
             double denom = 0.0;
             for (int64_t j = 0; j < n; ++j) {
                 if (!mask[j])
@@ -190,10 +194,16 @@ static int attn_rows_core(const uint16_t *q, const uint16_t *k, const uint16_t *
                 const uint16_t *vj = v + ((size_t)(off + j) * hkv + g) * d;
                 for (int32_t c = 0; c < d; ++c)
                     o[c] += p * widen_bf16(vj[c]);
+                if (aw)
+                    for (int32_t c = 0; c < d; ++c)
+                        aw[c] += p * fabs(widen_bf16(vj[c]));
             }
             if (denom > 0.0) {
                 for (int32_t c = 0; c < d; ++c)
                     o[c] /= denom;
+                if (aw)
+                    for (int32_t c = 0; c < d; ++c)
+                        aw[c] /= denom;
             }
             if (lse)
                 lse[r] = denom > 0.0 ? zmax + log(denom) : -INFINITY;
@@ -215,7 +225,21 @@ int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
         return -1;
     mask_src ms = {kind, sink, window, last, 0, NULL, NULL, NULL};
     return attn_rows_core(q, k, v, cu_seqlens, batch, hq, hkv, d, &ms, scale,
-                          row_tok, row_head, nrows, out, lse);
+                          row_tok, row_head, nrows, out, lse, NULL);
+}
+
+int oracle_attn_rows_absw(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                          const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                          int32_t hkv, int32_t d, int kind, int64_t sink,
+                          int64_t window, int64_t last, double scale,
+                          const int64_t *row_tok, const int32_t *row_head,
+                          int64_t nrows, double *out, double *lse, double *absw)
+{
+    if (kind != ORACLE_TRIANGLE && kind != ORACLE_CAUSAL)
+        return -1;
+    mask_src ms = {kind, sink, window, last, 0, NULL, NULL, NULL};
+    return attn_rows_core(q, k, v, cu_seqlens, batch, hq, hkv, d, &ms, scale,
+                          row_tok, row_head, nrows, out, lse, absw);
 }
 
 /* ---- Block-sparse causal attention ---- */
@@ -262,7 +286,7 @@ int oracle_attn_rows_bs(const uint16_t *q, const uint16_t *k, const uint16_t *v,
         return -1;
     mask_src ms = {-1, 0, 0, 0, tile, qtile_ptr, ktile_idx, base};
     const int rc = attn_rows_core(q, k, v, cu_seqlens, batch, hq, hkv, d, &ms,
-                                  scale, row_tok, row_head, nrows, out, lse);
+                                  scale, row_tok, row_head, nrows, out, lse, NULL);
     free(base);
     return rc;
 }

@@ -67,6 +67,21 @@ int oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
                      int64_t nrows, double *out, double *lse);
 
 /*
+ * oracle_attn_rows plus, per output element, the probability-weighted mean
+ * of |v| over the row's kept keys: absw[r * d + c] = sum_j p_j |v_jc|.  It
+ * bounds the error that rounding the probabilities to a narrower format
+ * can cause in a weighted sum of V: if each p_j carries a relative error of
+ * at most u, the output element moves by at most u * absw (numerator only;
+ * the normaliser is kept exact).
+ */
+int oracle_attn_rows_absw(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                          const int32_t *cu_seqlens, int32_t batch, int32_t hq,
+                          int32_t hkv, int32_t d, int kind, int64_t sink,
+                          int64_t window, int64_t last, double scale,
+                          const int64_t *row_tok, const int32_t *row_head,
+                          int64_t nrows, double *out, double *lse, double *absw);
+
+/*
  * Tile schedule by brute force: a (q-tile, k-tile) pair is kept iff some
  * (i, j) inside it is kept by oracle_mask.  Emitted in the documented packed
  * int32 format (header, main items, merge items).  Writes at most cap words

@@ -204,6 +204,63 @@ def _out_dtype(o):
     raise ValueError(f"o must be bf16 or fp32, got {o.dtype}")
 
 
+def _check_tensors(q, k, v, o, lse, sched_dev, info, workspace=None, extra=()):
+    """Validate what the C interface cannot see: dtypes, contiguity, shapes
+    and devices of the torch tensors whose raw pointers are passed.  Raises
+    ValueError before anything is enqueued (a wrong shape or a strided view
+    would otherwise be misread, or read out of bounds, by the kernels).
+    extra: (name, tensor, dtype, shape) of further operands."""
+    import torch
+    named = [("q", q), ("k", k), ("v", v), ("o", o)]
+    for name, t in named:
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name} must be a torch tensor")
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{name} must be bfloat16, got {t.dtype}")
+        if t.dim() != 3:
+            raise ValueError(f"{name} must be [tokens, heads, head_dim], got {tuple(t.shape)}")
+    _out_dtype(o)
+    total, hq, d = q.shape
+    if k.shape[0] != total or v.shape[0] != total:
+        raise ValueError(f"k and v must have {total} tokens like q, got "
+                         f"{k.shape[0]} and {v.shape[0]}")
+    if k.shape != v.shape:
+        raise ValueError(f"k {tuple(k.shape)} and v {tuple(v.shape)} differ")
+    if k.shape[2] != d:
+        raise ValueError(f"k/v head_dim {k.shape[2]} != q head_dim {d}")
+    if tuple(o.shape) != tuple(q.shape):
+        raise ValueError(f"o must have q's shape {tuple(q.shape)}, got {tuple(o.shape)}")
+    if lse is not None:
+        named.append(("lse", lse))
+        if lse.dtype != torch.float32 or tuple(lse.shape) != (hq, total):
+            raise ValueError(f"lse must be float32 [{hq}, {total}], got "
+                             f"{lse.dtype} {tuple(lse.shape)}")
+    named.append(("sched_dev", sched_dev))
+    if not isinstance(sched_dev, torch.Tensor) or sched_dev.dtype != torch.int32:
+        raise ValueError("sched_dev must be an int32 tensor of schedule words")
+    if sched_dev.numel() != info.words:
+        raise ValueError(f"sched_dev holds {sched_dev.numel()} words, the schedule "
+                         f"info says {info.words}")
+    if workspace is not None:
+        named.append(("workspace", workspace))
+    for name, t, dtype, shape in extra:
+        named.append((name, t))
+        if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must be {dtype} {tuple(shape)}, got "
+                             f"{t.dtype} {tuple(t.shape)}")
+    for name, t in named:
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    dev = q.device
+    for name, t in named:
+        if t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, q on {dev}: all operands "
+                             "must be on one device")
+    if dev.type != "cuda":
+        raise ValueError(f"operands must be on a GPU, got {dev}")
+
+
 def triangle_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
                       workspace, stream=None):
     """Enqueue Triangle attention on ``stream`` (torch current stream if None).
@@ -212,6 +269,7 @@ def triangle_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
     lse [Hq, T] fp32 or None; sched_dev int32 cuda tensor of the schedule
     words; workspace uint8 cuda tensor of >= ta_workspace_bytes bytes or None.
     """
+    _check_tensors(q, k, v, o, lse, sched_dev, info, workspace)
     total, hq, d = q.shape
     hkv = k.shape[1]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
@@ -224,6 +282,7 @@ def triangle_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
 def triangle_attn_tiles(q, k, v, o, lse, sched_dev, info, softmax_scale,
                         workspace, stream=None):
     """Enqueue the attention pass of Triangle attention (no merge)."""
+    _check_tensors(q, k, v, o, lse, sched_dev, info, workspace)
     total, hq, d = q.shape
     hkv = k.shape[1]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
@@ -235,7 +294,25 @@ def triangle_attn_tiles(q, k, v, o, lse, sched_dev, info, softmax_scale,
 
 def triangle_attn_merge(o, lse, sched_dev, info, workspace, stream=None):
     """Enqueue the merge of the Last-row split partials into o / lse."""
+    import torch
+    _out_dtype(o)
     total, hq, d = o.shape
+    named = [("o", o), ("sched_dev", sched_dev)]
+    if lse is not None:
+        named.append(("lse", lse))
+        if lse.dtype != torch.float32 or tuple(lse.shape) != (hq, total):
+            raise ValueError(f"lse must be float32 [{hq}, {total}]")
+    if workspace is not None:
+        named.append(("workspace", workspace))
+    if sched_dev.dtype != torch.int32 or sched_dev.numel() != info.words:
+        raise ValueError("sched_dev must hold the schedule's int32 words")
+    for name, t in named:
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.device != o.device:
+            raise ValueError(f"{name} is on {t.device}, o on {o.device}")
+    if o.device.type != "cuda":
+        raise ValueError(f"operands must be on a GPU, got {o.device}")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().triangle_attn_merge(
         _ptr(o), _out_dtype(o), _ptr(lse), _ptr(sched_dev), ctypes.byref(info),
@@ -245,6 +322,7 @@ def triangle_attn_merge(o, lse, sched_dev, info, workspace, stream=None):
 def blocksparse_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
                          workspace, stream=None):
     """Enqueue block-sparse causal attention (tiles + merge)."""
+    _check_tensors(q, k, v, o, lse, sched_dev, info, workspace)
     total, hq, d = q.shape
     hkv = k.shape[1]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
@@ -257,6 +335,7 @@ def blocksparse_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
 def causal_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
                     stream=None):
     """Enqueue dense causal attention on ``stream``; arguments as above."""
+    _check_tensors(q, k, v, o, lse, sched_dev, info)
     total, hq, d = q.shape
     hkv = k.shape[1]
     _check(lib().causal_attn_fwd(
@@ -279,6 +358,13 @@ def region_grad_probe(q, k, v, dout, lse, sched_dev, info, softmax_scale, sink,
     per-head sums of A_ij <dO_i, V_j>; workspace uint8 cuda tensor of >=
     ta_probe_workspace_bytes bytes or None.
     """
+    import torch
+    if lse is None:
+        raise ValueError("the probe needs the causal LSE [Hq, T]")
+    if not isinstance(dout, torch.Tensor) or dout.dtype != torch.bfloat16:
+        raise ValueError(f"dout must be a bfloat16 tensor, got {getattr(dout, 'dtype', dout)}")
+    _check_tensors(q, k, v, dout, lse, sched_dev, info, workspace,
+                   extra=(("region_sums", region_sums, torch.float64, (q.shape[1], 3)),))
     total, hq, d = q.shape
     hkv = k.shape[1]
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()

@@ -1074,9 +1074,10 @@ ta_status check_common(const char *fn, int want_kind, const void *q, const void 
     const int64_t subtiles = info->tile / rows_per_wg(hq / hkv, info->tile);
     if ((int64_t)info->n_items * subtiles * hkv > INT32_MAX)
         return fail(TA_ERR_UNSUPPORTED, "%s: grid too large", fn);
-    // per-lane copy offsets use 24-bit multiplies of the key row pitch
-    if (2LL * hkv * head_dim >= (1LL << 24))
-        return fail(TA_ERR_UNSUPPORTED, "%s: hkv * head_dim too large", fn);
+    // per-lane copy offsets use 24-bit multiplies of the K/V and Q row
+    // pitches (2 hkv d and 2 hq d bytes; hq >= hkv)
+    if (2LL * hq * head_dim >= (1LL << 24))
+        return fail(TA_ERR_UNSUPPORTED, "%s: hq * head_dim too large", fn);
     return TA_OK;
 }
 

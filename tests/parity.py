@@ -66,27 +66,45 @@ def sample_rows(cu, sink, window, last, tile, n_random, seed, all_last=True):
     return np.array(sorted(toks), dtype=np.int64)
 
 
-def bf16_p_bound(v_cpu):
-    """Largest output error the bf16 rounding of the probabilities can cause:
-    |sum_j dp_j v_j| / sum_j p_j <= 2^-8 max_j |v_j| (round-to-nearest bf16
-    has relative error <= 2^-8).  Rows with few keys can reach it."""
-    return 2.0 ** -8 * float(v_cpu.float().abs().max())
+# Rounding the probabilities to bf16 for the PV product (round to nearest
+# even, 8 significant bits) changes each p_j by a relative error of at most
+# u = 2^-8, while the normaliser l sums the unrounded fp32 values.  The
+# output error of element (i, c) is then sum_j (p'_j - p_j) v_jc / l, at most
+# u * sum_j p_j |v_jc| / l = u * absw_ic, a weighted mean of |v| that the
+# oracle computes.  Spread-out rows average the rounding errors away (max-abs
+# a few 1e-3); rows dominated by one key of large |v| can approach u |v|.
+# The factor 1 + 2^-6 covers the fp32 logits, exp2 and accumulation.
+P_ROUND_U = 2.0 ** -8
+P_BOUND_FACTOR = P_ROUND_U * (1.0 + 2.0 ** -6)
+P_BOUND_ABS = 1e-5
 
 
 def compare(kind, q_cpu, k_cpu, v_cpu, cu, sink, window, last, scale, o, lse,
-            toks, heads, label="", max_abs=MAX_ABS):
-    """Check GPU rows o[toks, h] (fp32/bf16 cuda) against the oracle."""
+            toks, heads, label="", max_abs=MAX_ABS, p_bound=False):
+    """Check GPU rows o[toks, h] (fp32/bf16 cuda) against the oracle.
+
+    With ``p_bound`` an element may exceed ``max_abs`` only up to the bf16
+    probability-rounding bound of that element (P_BOUND_FACTOR * absw +
+    P_BOUND_ABS); relative L2 and LSE keep the flat bar."""
     toks = np.asarray(toks, dtype=np.int64)
     heads = list(heads)
     rt = np.repeat(toks, len(heads))
     rh = np.tile(np.array(heads, dtype=np.int32), toks.size)
-    ref_o, ref_lse = oracle.attn_rows(q_cpu, k_cpu, v_cpu, cu, kind, sink,
-                                      window, last, scale, rt, rh)
+    if p_bound:
+        ref_o, ref_lse, absw = oracle.attn_rows(q_cpu, k_cpu, v_cpu, cu, kind, sink,
+                                                window, last, scale, rt, rh,
+                                                with_absw=True)
+        tol = np.maximum(max_abs, P_BOUND_FACTOR * absw + P_BOUND_ABS)
+    else:
+        ref_o, ref_lse = oracle.attn_rows(q_cpu, k_cpu, v_cpu, cu, kind, sink,
+                                          window, last, scale, rt, rh)
+        tol = np.full(ref_o.shape, max_abs)
     idx_t = torch.from_numpy(rt).to(o.device)
     idx_h = torch.from_numpy(rh.astype(np.int64)).to(o.device)
     got_o = o[idx_t, idx_h].double().cpu().numpy()
     got_lse = lse[idx_h, idx_t].double().cpu().numpy()
     worst = {}
+    over_flat = 0
     for h in heads:
         sel = rh == h
         err = got_o[sel] - ref_o[sel]
@@ -94,8 +112,10 @@ def compare(kind, q_cpu, k_cpu, v_cpu, cu, sink, window, last, scale, o, lse,
         rel = float(np.linalg.norm(err) / max(np.linalg.norm(ref_o[sel]), 1e-30))
         lse_err = float(np.abs(got_lse[sel] - ref_lse[sel]).max())
         worst[h] = (max_err, rel, lse_err)
-        if not (max_err <= max_abs and rel <= REL_L2 and lse_err <= LSE_ABS):
-            bad = np.argwhere(np.abs(err) > max_abs)
+        elem_ok = bool((np.abs(err) <= tol[sel]).all())
+        over_flat += int((np.abs(err) > MAX_ABS).sum())
+        if not (elem_ok and rel <= REL_L2 and lse_err <= LSE_ABS):
+            bad = np.argwhere(np.abs(err) > tol[sel])
             rows = sorted(set(int(rt[sel][i]) for i, _ in bad[:20]))
             raise AssertionError(
                 f"{label} head {h}: max-abs {max_err:.3e}, rel-L2 {rel:.3e}, "
@@ -103,5 +123,7 @@ def compare(kind, q_cpu, k_cpu, v_cpu, cu, sink, window, last, scale, o, lse,
     log(f"{label}: {len(toks)} rows x {len(heads)} heads, worst max-abs "
         f"{max(w[0] for w in worst.values()):.2e} rel-L2 "
         f"{max(w[1] for w in worst.values()):.2e} lse "
-        f"{max(w[2] for w in worst.values()):.2e}")
+        f"{max(w[2] for w in worst.values()):.2e}"
+        + (f"; {over_flat} elements above {MAX_ABS:g}, within the bf16-P bound"
+           if over_flat else ""))
     return worst

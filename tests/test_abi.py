@@ -138,6 +138,11 @@ def test_fwd_rejects_bad_arguments_without_launching():
     bad.tile = 32
     assert _fwd(info=bad) == B.TA_ERR_UNSUPPORTED
     assert _fwd("causal", info=cau, d=80) == B.TA_ERR_UNSUPPORTED
+    # row pitches of Q (2 hq d bytes) and K/V must stay below 2^24 bytes:
+    # hq 65536 with d 128 is rejected even though hkv alone would pass
+    assert _fwd(info=tri, hq=65536, hkv=8192) == B.TA_ERR_UNSUPPORTED
+    assert "hq * head_dim" in B.ta_last_error()
+    assert _fwd("causal", info=cau, hq=65536, hkv=8192) == B.TA_ERR_UNSUPPORTED
     # the word count must match the items (and a block-sparse list section)
     bad = B.ScheduleInfo.from_buffer_copy(tri)
     bad.words += 1
@@ -150,6 +155,68 @@ def test_fwd_rejects_bad_arguments_without_launching():
         bad = B.ScheduleInfo.from_buffer_copy(bs)
         setattr(bad, field, getattr(bad, field) + delta)
         assert _fwd("blocksparse", info=bad) == B.TA_ERR_SCHEDULE_MISMATCH, field
+
+
+def _host_tensors(total=100, hq=8, hkv=2, d=128):
+    import torch
+    q = torch.zeros((total, hq, d), dtype=torch.bfloat16)
+    k = torch.zeros((total, hkv, d), dtype=torch.bfloat16)
+    v = torch.zeros((total, hkv, d), dtype=torch.bfloat16)
+    o = torch.zeros((total, hq, d), dtype=torch.float32)
+    lse = torch.zeros((hq, total), dtype=torch.float32)
+    return q, k, v, o, lse
+
+
+def test_binding_rejects_bad_tensors_before_any_gpu_call():
+    """The binding checks dtypes, contiguity, shapes and devices of the
+    tensors whose raw pointers it passes; every case here is CPU tensors
+    and fails in Python before anything is enqueued."""
+    import torch
+    words, info = B.ta_build_schedule("triangle", [0, 100], 4, 8, 2, 64)
+    sched = torch.from_numpy(words)
+    ws = torch.zeros(B.ta_workspace_bytes(info, 8, 128), dtype=torch.uint8)
+
+    def call(q, k, v, o, lse, s=sched, fn=B.triangle_attn_fwd):
+        fn(q, k, v, o, lse, s, info, 0.1, ws)
+
+    q, k, v, o, lse = _host_tensors()
+    cases = {
+        "q must be bfloat16": (q.half(), k, v, o, lse),
+        "k must be bfloat16": (q, k.float(), v, o, lse),
+        "v must be [tokens": (q, k, v[0], o, lse),
+        "k and v must have 100 tokens": (q, k[:99], v[:99], o, lse),
+        "differ": (q, k, v[:, :1], o, lse),
+        "head_dim 64": (q, k[..., :64], v[..., :64], o, lse),
+        "o must have q's shape": (q, k, v, o[:50], lse),
+        "o must be bf16 or fp32": (q, k, v, o.half(), lse),
+        "lse must be float32": (q, k, v, o, lse.T.contiguous()),
+        "q must be contiguous": (q.transpose(0, 1).contiguous().transpose(0, 1), k, v, o, lse),
+        "k must be contiguous": (q, torch.zeros((100, 4, 128), dtype=torch.bfloat16)[:, ::2],
+                                 v, o, lse),
+        "operands must be on a GPU": (q, k, v, o, lse),
+    }
+    for msg, args in cases.items():
+        with pytest.raises(ValueError, match=re.escape(msg)):
+            call(*args)
+    with pytest.raises(ValueError, match="sched_dev holds"):
+        call(q, k, v, o, lse, s=sched[:-1])
+    with pytest.raises(ValueError, match="int32"):
+        call(q, k, v, o, lse, s=sched.long())
+    for fn in (B.triangle_attn_tiles, B.blocksparse_attn_fwd):
+        with pytest.raises(ValueError, match="k and v must have"):
+            call(q, k[:99], v[:99], o, lse, fn=fn)
+    _, cinfo = B.ta_build_schedule("causal", [0, 100], 4, 8, 2, 64)
+    with pytest.raises(ValueError, match="o must have"):
+        B.causal_attn_fwd(q, k, v, o[:, :4], lse, sched, cinfo, 0.1)
+    with pytest.raises(ValueError, match="lse must be"):
+        B.triangle_attn_merge(o, lse[:4], sched, info, ws)
+    with pytest.raises(ValueError, match="must be on a GPU"):
+        B.triangle_attn_merge(o, lse, sched, info, ws)
+    sums = torch.zeros((8, 3), dtype=torch.float64)
+    with pytest.raises(ValueError, match="region_sums"):
+        B.region_grad_probe(q, k, v, q, lse, sched, info, 0.1, 4, 8, 2, sums[:4], ws)
+    with pytest.raises(ValueError, match="dout must be"):
+        B.region_grad_probe(q, k, v, q.float(), lse, sched, info, 0.1, 4, 8, 2, sums, ws)
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

@@ -17,7 +17,7 @@ import pytest
 import torch
 
 from paper_2507_21526_amd.inputs import draw_qkv
-from tests.parity import bf16_p_bound, compare, log, run_pass
+from tests.parity import compare, log, run_pass
 
 pytestmark = pytest.mark.gpu
 
@@ -36,8 +36,11 @@ def _check(kind, q, k, v, scale, label):
                          poison=True)
     torch.cuda.synchronize()
     assert not torch.isnan(o).any(), f"{label}: unwritten or NaN output rows"
+    # Peaked rows (one key far above the rest) are where the bf16 rounding of
+    # the probabilities shows: an element may exceed 1e-2 only within its own
+    # rounding bound 2^-8 sum_j p_j |v_j| (tests/parity.py).
     compare(kind, q, k, v, CU, S, W, L, scale, o, lse, np.arange(CU[-1]),
-            range(HQ), label=label, max_abs=bf16_p_bound(v))
+            range(HQ), label=label, p_bound=True)
 
 
 @pytest.mark.parametrize("kind", ["triangle", "causal"])

@@ -25,8 +25,11 @@ def _heads(hq, hkv, seed):
 
 
 def _check_workload(name, layer=0, kinds=("triangle", "causal"), n_random=96,
-                    shape=None):
-    """shape: optional (sink, window, last) replacing the workload's own."""
+                    shape=None, bf16_out=False):
+    """shape: optional (sink, window, last) replacing the workload's own.
+    bf16_out: also run the bf16 output mode (the one the benchmark times) and
+    require every element to equal the fp32 output rounded to nearest even
+    within one bf16 ulp, with identical LSE."""
     w = WORKLOADS[name]
     cu = list(w.cu_seqlens)
     sink, window, last = shape if shape else (w.sink, w.window, w.last)
@@ -46,6 +49,20 @@ def _check_workload(name, layer=0, kinds=("triangle", "causal"), n_random=96,
                            all_last=(kind == "triangle"))
         compare(kind, q, k, v, cu, sink, window, last, w.scale, o, lse,
                 rows, heads, label=f"{name} layer {layer} {kind} S/W/L={sink}/{window}/{last}")
+        if bf16_out:
+            o16 = torch.empty(o.shape, dtype=torch.bfloat16, device=o.device)
+            l16 = torch.empty_like(lse)
+            plan.run(qg, kg, vg, o16, l16, w.scale)
+            torch.cuda.synchronize()
+            ref = o.to(torch.bfloat16)
+            diff = (o16.view(torch.int16).int() - ref.view(torch.int16).int()).abs()
+            worst = int(diff.max())
+            log(f"{name} {kind}: bf16 output vs RNE(fp32 output) on all "
+                f"{o16.numel()} elements: max {worst} ulp, "
+                f"{int((diff > 0).sum())} differ")
+            assert worst <= 1, (name, kind, worst)
+            assert torch.equal(l16, lse), (name, kind)
+            del o16, l16, ref, diff
         del o, lse, plan
     del qg, kg, vg
     torch.cuda.empty_cache()
@@ -56,7 +73,7 @@ def test_llama_32k():
 
 
 def test_llama_128k():
-    _check_workload("llama8b_n128k")
+    _check_workload("llama8b_n128k", bf16_out=True)
 
 
 def test_llama_varlen():

@@ -131,6 +131,33 @@ def test_oracle_matches_sdpa_fp64(kind, cu, hq, hkv, d, S, W, L):
     np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("kind", ["triangle", "causal"])
+def test_oracle_absw_is_attention_over_abs_v(kind):
+    """The probability-weighted mean of |v| that bounds the bf16 rounding of
+    the probabilities is attention with V replaced by |V|: torch SDPA in
+    float64 over |V| computes it independently.  Also: row 0 (one key) gives
+    |v_0|, and absw >= |out| everywhere."""
+    cu = [0, 150, 333]
+    hq, hkv, d, S, W, L = 6, 2, 64, 5, 40, 20
+    q, k, v = draw_qkv(cu, hq, hkv, d, seed=77)
+    scale = 1.0 / math.sqrt(d)
+    toks = np.repeat(np.arange(cu[-1], dtype=np.int64), hq)
+    heads = np.tile(np.arange(hq, dtype=np.int32), cu[-1])
+    out, lse, absw = oracle.attn_rows(q, k, v, cu, kind, S, W, L, scale, toks,
+                                      heads, with_absw=True)
+    ref = _sdpa_ref(q, k, v.abs(), cu, kind, S, W, L, scale).reshape(-1, d)
+    np.testing.assert_allclose(absw, ref, rtol=1e-12, atol=1e-12)
+    out_plain, lse_plain = oracle.attn_rows(q, k, v, cu, kind, S, W, L, scale,
+                                            toks, heads)
+    np.testing.assert_array_equal(out, out_plain)
+    np.testing.assert_array_equal(lse, lse_plain)
+    assert (absw >= np.abs(out) - 1e-15).all()
+    for s in cu[:-1]:
+        sel = toks == s
+        np.testing.assert_array_equal(
+            absw[sel], np.abs(v[s].double().numpy()).repeat(hq // hkv, axis=0))
+
+
 def test_oracle_matches_textbook_softmax():
     """exp / sum without the max shift, on small logits, in numpy fp64."""
     cu = [0, 40]
