@@ -9,12 +9,18 @@ timing starts (the schedule is built once per (cu_seqlens, S, W, L, tile)
 on the host; its build time is reported separately).  The dense causal
 forward on the same inputs is timed with the same protocol for the speedup.
 
+Timing protocol: W warm-up steps, then K steps each preceded by a 1 GiB
+device write that evicts L2 and the 256 MB MALL; ms_per_step is the median
+of the K per-step HIP event times.  The same K steps back to back (warm
+caches) are reported in step_stats.
+
 Prints ONE JSON line on stdout (logs go to stderr):
   value     = kept-tile FLOPs / ms_per_step, in TFLOP/s (kept-tile FLOPs =
               kept (q-tile, k-tile) pairs x Hq x 4 T^2 d)
   roofline  = the tile kernel (dominant): kept-tile FLOPs per launch over its
-              mean launch time from HIP events on the launch stream, against
-              the bf16 dense MFMA peak of MI355X (2.5 PFLOP/s)
+              mean launch time over the K flushed steps (HIP events on the
+              launch stream), against the bf16 dense MFMA peak of MI355X
+              (2.5 PFLOP/s)
   cpu_baseline = the fp64 oracle on the host cores, timed on a bounded row
               sample of the same workload and extrapolated per row class.
 """
@@ -66,9 +72,11 @@ def kernel_source_hash(texts=None) -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str):
-    """HBM bytes per tile-kernel launch from committed rocprofv3 counter runs,
-    or None when absent or taken on another version of the kernel source."""
+def load_traffic(workload: str, which: str = "tile"):
+    """HBM bytes per tile-kernel launch (which="tile"), or the merge kernel's
+    fetched and written bytes per launch (which="merge", a dict), from
+    committed rocprofv3 counter runs; None when absent or taken on another
+    version of the kernel source."""
     path = os.path.join(ROOT, "profiles", f"traffic_tile_kernel_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -76,10 +84,13 @@ def load_traffic(workload: str):
         rec = json.load(f)
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
+    if which == "merge":
+        return rec.get("merge")
     return rec.get("hbm_bytes_per_launch")
 
 
 COPY_BYTES = 1 << 30  # bytes read (and written) by the calibration copy
+FLUSH_BYTES = 1 << 30  # device write that evicts L2 and the MALL before a rep
 TILE_KERNEL = "attn_tile_kernel"
 MERGE_KERNEL = "merge_kernel"
 
@@ -152,12 +163,16 @@ def summarize(root, workload):
                         groups.setdefault(key, []).append(
                             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
             out.write("| kernel | workgroups | calls | average ms | min ms | average of "
-                      "the timed calls ms |\n")
+                      "the timed (flushed) calls ms |\n")
             out.write("|---|---|---|---|---|---|\n")
             for (k, wgs), v in sorted(groups.items()):
-                # timed calls: the last `steps` of the Triangle pass (after
-                # `warmup`), the dense pass's calls after its one warm-up
-                tail = v[-steps:] if len(v) >= steps + warmup else v[1:] or v
+                # timed calls: the Triangle pass runs `warmup` steps, `steps`
+                # flushed (timed) steps, then `steps` warm ones; the dense
+                # pass one warm-up, then its flushed steps
+                if len(v) >= warmup + 2 * steps:
+                    tail = v[warmup:warmup + steps]
+                else:
+                    tail = v[1:] or v
                 out.write(f"| {k} | {wgs} | {len(v)} | {sum(v) / len(v):.4f} | "
                           f"{min(v):.4f} | {sum(tail) / len(tail):.4f} |\n")
             out.write("\nFor llama8b_n128k the Triangle tile pass launches "
@@ -176,6 +191,8 @@ def summarize(root, workload):
         w_copy = pick(write, copy_key)
         f_tile = pick(fetch, TILE_KERNEL)
         w_tile = pick(write, TILE_KERNEL)
+        f_merge = pick(fetch, MERGE_KERNEL)
+        w_merge = pick(write, MERGE_KERNEL)
         f_fac = f_copy * 1024.0 / COPY_BYTES    # counter KiB per real byte
         w_fac = w_copy * 1024.0 / COPY_BYTES
         rec = {
@@ -188,6 +205,11 @@ def summarize(root, workload):
             "copy_bytes": COPY_BYTES,
             "fetch_factor": f_fac, "write_factor": w_fac,
             "hbm_bytes_per_launch": (f_tile / f_fac + w_tile / w_fac) * 1024.0,
+            "merge": ({"kernel": MERGE_KERNEL,
+                       "fetch_kib_per_launch": f_merge, "write_kib_per_launch": w_merge,
+                       "fetch_bytes": f_merge / f_fac * 1024.0,
+                       "write_bytes": w_merge / w_fac * 1024.0}
+                      if f_merge is not None and w_merge is not None else None),
             "commands": [
                 "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir>/fetch "
                 f"-- python3 bench.py --workload {workload} --steps 1 --warmup 0 "
@@ -317,6 +339,35 @@ def timed_pass(binding, plan, q, k, v, o, scale, stream, steps, warmup, torch):
     return e0.elapsed_time(e1) / steps
 
 
+_FLUSH = {}
+
+
+def flush_caches(dev, torch, i=0):
+    """Evict L2 and the 256 MB MALL: a 1 GiB device write on the current
+    stream (the next launch on that stream starts after it)."""
+    buf = _FLUSH.get(dev)
+    if buf is None:
+        buf = _FLUSH[dev] = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    buf.fill_(i & 0xFF)
+
+
+def flushed_pass(binding, plan, q, k, v, o, scale, stream, reps, torch):
+    """Median time (ms, HIP events) of one full pass, each of `reps` passes
+    preceded by a cache flush."""
+    import numpy as np
+    times = []
+    for i in range(reps):
+        flush_caches(q.device, torch, i)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        plan.run(q, k, v, o, None, scale, stream)
+        e1.record(stream)
+        times.append((e0, e1))
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in times]))
+
+
 def element_exact(binding, cu, w, d, ms):
     """FLOPs of the kept (row, key) pairs alone: 4 d per pair and query head,
     pairs per head from the closed-form section counts."""
@@ -331,7 +382,7 @@ def kept_flops(info, hq, tile, d):
 
 
 def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, torch,
-                   only=None):
+                   only=None, main_qkv=None):
     """Timing of the other workloads: the 32K Llama layer, the varlen batch (per-sequence
     schedules), the 28-layer Qwen stack (mixed vs all-dense), block-sparse
     causal attention on the 128K Llama layer, that layer at the paper's own
@@ -340,28 +391,41 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
     tokens."""
     import numpy as np
 
-    from paper_2507_21526_amd.inputs import blocksparse_lists
+    from paper_2507_21526_amd.inputs import blocksparse_lists, workload_qkv
     stream = torch.cuda.current_stream()
     out = {}
+
+    def llama128k_qkv():
+        # the 128K Llama layer's own inputs (key 0 with 8x norm), shared with
+        # the headline step when it ran in this process
+        if main_qkv is not None:
+            return main_qkv
+        return tuple(t.to(dev) for t in workload_qkv(WORKLOADS["llama8b_n128k"]))
 
     def want(name):
         return only is None or name in only
 
     if want("n32k"):
-        # the Llama layer at 32K tokens (per-head scales do not change timing)
+        # the Llama layer at 32K tokens on its own seeded inputs (per-head
+        # scales U[0.5, 2] widen the logit range; the lazy re-base of the
+        # online softmax depends on the values); its K and V (134 MB) fit in
+        # the 256 MB MALL, so it is also timed with L2 and MALL flushed
         w = WORKLOADS["llama8b_n32k"]
         cu = list(w.cu_seqlens)
-        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        q, k, v = (t.to(dev) for t in workload_qkv(w))
         o = torch.empty_like(q)
         tri = binding.Plan("triangle", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
                            device=dev)
         den = binding.Plan("causal", cu, w.sink, w.window, w.last, w.tile, w.hq, w.d,
                            device=dev)
         t_tri = timed_pass(binding, tri, q, k, v, o, w.scale, stream, 20, 3, torch)
+        t_tri_cold = flushed_pass(binding, tri, q, k, v, o, w.scale, stream, 20, torch)
         t_den = timed_pass(binding, den, q, k, v, o, w.scale, stream, 5, 1, torch)
         out["n32k"] = {
-            "workload": w.name, "cu_seqlens": cu,
-            "triangle_ms": t_tri, "dense_ms": t_den,
+            "workload": w.name, "cu_seqlens": cu, "inputs": "the workload's own "
+            "(numpy PCG64 seed 1002, per-head scales)",
+            "triangle_ms": t_tri, "triangle_flushed_median_ms": t_tri_cold,
+            "dense_ms": t_den,
             "triangle_kept_tile_tflops": kept_flops(tri.info, w.hq, w.tile, w.d) / t_tri / 1e9,
             "dense_kept_tile_tflops": kept_flops(den.info, w.hq, w.tile, w.d) / t_den / 1e9,
             "speedup_vs_dense": t_den / t_tri,
@@ -440,7 +504,7 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         cu = list(w.cu_seqlens)
         nq = -(-cu[-1] // w.tile)
         ptr, idx = blocksparse_lists(nq, 0.1, w.seed)
-        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        q, k, v = llama128k_qkv()
         o = torch.empty_like(q)
         bs = binding.Plan("blocksparse", cu, 0, 1, 0, w.tile, w.hq, w.d, device=dev,
                           blocks=(ptr, idx))
@@ -460,7 +524,7 @@ def extra_sections(binding, WORKLOADS, triangle_layer_set, dense_128k_ms, dev, t
         # the paper's Streaming shape on the 128K Llama layer
         w = WORKLOADS["llama8b_n128k"]
         cu = list(w.cu_seqlens)
-        q, k, v = gpu_qkv(cu[-1], w.hq, w.hkv, w.d, w.seed, dev, torch)
+        q, k, v = llama128k_qkv()
         o = torch.empty_like(q)
         ps = binding.Plan("triangle", cu, 8, 512, w.last, w.tile, w.hq, w.d, device=dev)
         t_ps = timed_pass(binding, ps, q, k, v, o, w.scale, stream, 10, 2, torch)
@@ -637,29 +701,45 @@ def main():
             ev[1].record(stream)
             ev[2].record(stream)
 
-    log(f"timing Triangle: {args.warmup} warmup + {args.steps} steps")
-    wall, events = time_loop(tri_step, args.steps, args.warmup, torch)
+    # Timed protocol: W warm-up steps, then exactly K steps, each preceded by
+    # a 1 GiB device write that evicts L2 and the 256 MB MALL (on the same
+    # stream, so the step starts when the write ends and the GPU never idles
+    # in between); per-step times from HIP events on the launch stream.  The
+    # same K steps back to back (warm caches) are reported beside them.
+    log(f"timing Triangle: {args.warmup} warmup + {args.steps} flushed steps")
+    for _ in range(args.warmup):
+        tri_step(None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    events = []
+    for i in range(args.steps):
+        flush_caches(dev, torch, i)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        tri_step(ev)
+        events.append(ev)
+    torch.cuda.synchronize()
+    flushed_wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    step_times = [e[0].elapsed_time(e[2]) for e in events]
     tile_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     merge_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events]))
-    ms_per_step = wall * 1e3
-    step_q = np.percentile([e[0].elapsed_time(e[2]) for e in events], [25, 50, 75])
-    step_stats = {"warm_median_ms": float(step_q[1]),
-                  "warm_iqr_ms": float(step_q[2] - step_q[0])}
-    if not args.no_extra:
-        # cold steps: L2 and the 256 MB MALL flushed by a 1 GiB device write
-        # before each (same stream, so the write ends before the step starts)
-        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        cold = []
-        for i in range(5):
-            flush.fill_(i)
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-            tri_step(ev)
-            cold.append(ev)
-        torch.cuda.synchronize()
-        cq = np.percentile([e[0].elapsed_time(e[2]) for e in cold], [25, 50, 75])
-        step_stats.update({"cold_median_ms": float(cq[1]), "cold_iqr_ms": float(cq[2] - cq[0]),
-                           "cold_steps": len(cold)})
-        del flush
+    step_q = np.percentile(step_times, [25, 50, 75])
+    ms_per_step = float(step_q[1])
+    log(f"timing Triangle: {args.steps} warm steps back to back")
+    wall, wevents = time_loop(tri_step, args.steps, 0, torch)
+    warm_q = np.percentile([e[0].elapsed_time(e[2]) for e in wevents], [25, 50, 75])
+    step_stats = {
+        "protocol": "each timed step preceded by a 1 GiB device write (L2 and MALL "
+                    "flushed); ms_per_step = median of the per-step HIP event times",
+        "flushed_median_ms": ms_per_step,
+        "flushed_iqr_ms": float(step_q[2] - step_q[0]),
+        "flushed_min_ms": float(min(step_times)), "flushed_max_ms": float(max(step_times)),
+        "flushed_steps": len(step_times),
+        "flushed_wall_ms_per_iteration_incl_flush": flushed_wall_ms,
+        "tile_kernel_mean_ms": tile_ms, "merge_kernel_mean_ms": merge_ms,
+        "warm_median_ms": float(warm_q[1]), "warm_iqr_ms": float(warm_q[2] - warm_q[0]),
+        "warm_wall_ms_per_step": wall * 1e3,
+        "warm_tile_kernel_mean_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in wevents])),
+    }
 
     T, d = w.tile, w.d
     kept_flops = float(info.kept_tiles_per_qhead) * w.hq * 4.0 * T * T * d
@@ -674,12 +754,20 @@ def main():
 
     dense_rec = None
     if not args.no_dense:
-        log(f"timing dense causal: 1 warmup + {args.dense_steps} steps")
-        dwall, devents = time_loop(dense_step, args.dense_steps, 1, torch)
-        dense_ms = dwall * 1e3
+        log(f"timing dense causal: 1 warmup + {args.dense_steps} flushed steps")
+        dense_step(None)
+        devents = []
+        for i in range(args.dense_steps):
+            flush_caches(dev, torch, i)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            dense_step(ev)
+            devents.append(ev)
+        torch.cuda.synchronize()
+        dense_ms = float(np.median([e[0].elapsed_time(e[1]) for e in devents]))
         dense_flops = float(dense.info.kept_tiles_per_qhead) * w.hq * 4.0 * T * T * d
         dense_rec = {
             "ms_per_step": dense_ms,
+            "protocol": "median of flushed steps, as the Triangle step",
             "kernel_ms": float(np.mean([e[0].elapsed_time(e[1]) for e in devents])),
             "kept_tile_tflops": dense_flops / (dense_ms * 1e-3) / 1e12,
             "frac_of_bf16_peak": dense_flops / (dense_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
@@ -694,9 +782,25 @@ def main():
     if not args.no_extra:
         log("timing the varlen batch, the 28-layer stack and the paper shape")
         extra = extra_sections(binding, WORKLOADS, triangle_layer_set,
-                               dense_rec["ms_per_step"] if dense_rec else None, dev, torch)
+                               dense_rec["ms_per_step"] if dense_rec else None, dev, torch,
+                               main_qkv=(qg, kg, vg))
 
     traffic = load_traffic(w.name)
+    merge_traffic = load_traffic(w.name, "merge")
+    merge_rec = {"kernel_ms": merge_ms, "algorithmic_bytes": merge_bytes,
+                 "gbs": merge_gbs,
+                 "frac_of_hbm_peak": (merge_gbs / PEAK_HBM_GBS) if merge_gbs else None}
+    if merge_traffic:
+        cb = merge_traffic["fetch_bytes"] + merge_traffic["write_bytes"]
+        merge_rec.update({
+            "counter_fetch_bytes": merge_traffic["fetch_bytes"],
+            "counter_write_bytes": merge_traffic["write_bytes"],
+            "counter_gbs": cb / (merge_ms * 1e-3) / 1e9,
+            "counter_note": "FETCH_SIZE / WRITE_SIZE count traffic between L2 and "
+                            "the memory fabric, MALL hits included: the partials were "
+                            "written by the tile kernel just before and are largely "
+                            "served from the 256 MB MALL",
+        })
     rec = {
         "metric": "Triangle-attn prefill TFLOP/s (kept tiles) + speedup vs dense causal @128K",
         "value": value,
@@ -731,9 +835,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "step_stats": step_stats,
-        "merge": {"kernel_ms": merge_ms, "algorithmic_bytes": merge_bytes,
-                  "gbs": merge_gbs, "frac_of_hbm_peak":
-                  (merge_gbs / PEAK_HBM_GBS) if merge_gbs else None},
+        "merge": merge_rec,
         # the same step counted on the (row, key) pairs the Triangle mask keeps
         # (streaming and Last sections, closed form) instead of whole tiles
         "element_exact": element_exact(binding, cu, w, d, ms_per_step),

@@ -104,6 +104,32 @@ __device__ __forceinline__ bool header_ok(const int32_t *s, int64_t total,
            t == total && s[H_ITEMS] == n_items;
 }
 
+// A schedule that does not match the launch (wrong header, malformed item)
+// leaves the workgroup without rows it can trust: every workgroup that finds
+// one fills its slice of O (and of LSE) with NaN instead, the slices of the
+// whole grid together covering every element, so that the caller sees the
+// failure in the output (Appendix A.1 initialises O before the loops; here
+// a rejected schedule leaves it NaN, not stale).  Vector stores only.
+__device__ __forceinline__ void poison_outputs(void *o, int o_f32, float *lse,
+                                            int64_t total_tokens, int32_t hq, int d,
+                                            int64_t block, int64_t n_blocks)
+{
+    const int64_t n_o = total_tokens * hq * d;
+    const int64_t n_l = lse ? total_tokens * hq : 0;
+    const int64_t co = (n_o + n_blocks - 1) / n_blocks;
+    const int64_t cl = (n_l + n_blocks - 1) / n_blocks;
+    const int64_t o0 = block * co, o1 = min(o0 + co, n_o);
+    const int64_t l0 = block * cl, l1 = min(l0 + cl, n_l);
+    for (int64_t i = o0 + threadIdx.x; i < o1; i += blockDim.x) {
+        if (o_f32)
+            reinterpret_cast<float *>(o)[i] = __builtin_nanf("");
+        else
+            reinterpret_cast<uint16_t *>(o)[i] = 0x7fc0;  // bf16 quiet NaN
+    }
+    for (int64_t i = l0 + threadIdx.x; i < l1; i += blockDim.x)
+        lse[i] = __builtin_nanf("");
+}
+
 // Key offset (within a 32-key block) held by register v of lane half h in
 // the S^T accumulator, given the permuted K row order.
 __device__ __forceinline__ int key_of_reg(int v, int h)
@@ -270,21 +296,23 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     const int32_t kb0 = it[I_KB0], kb1 = it[I_KB1];
     const int32_t mode = it[I_MODE];
     const int32_t part_base = it[I_PART_BASE];
-    if (!header_ok(sched, a.total_tokens, a.n_items, kind))
-        return;
-    // block-sparse schedules record the length of their k-tile lists
-    if (a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0))
-        return;
-    // Guard against a malformed schedule: never touch memory outside it.
-    // List items (kModeCausalList) read the k-tiles list[ka0 .. ka0 + ka1)
-    // of the tile-list section instead of two runs.
+    // Guard against a schedule that does not match the launch, and against a
+    // malformed item: never touch memory outside it; poison the outputs.
+    // Block-sparse schedules record the length of their k-tile lists.  List
+    // items (kModeCausalList) read the k-tiles list[ka0 .. ka0 + ka1) of the
+    // tile-list section instead of two runs.
     const bool list_mode = mode == kModeCausalList;
-    if (seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
+    if (!header_ok(sched, a.total_tokens, a.n_items, kind) ||
+        a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0) ||
+        seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
         r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || kb0 < 0 || kb1 < kb0 ||
         (list_mode ? (ka1 < 0 || kb1 != kb0 || (int64_t)ka0 + ka1 > a.list_words)
                    : ka1 < ka0) ||
-        (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows))
+        (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows)) {
+        poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x,
+                       gridDim.x);
         return;
+    }
     const int32_t *tile_list = sched + a.list_base + (list_mode ? ka0 : 0);
     const int max_ktile = seq_len > 0 ? (seq_len - 1) / a.tile : 0;
 
@@ -884,15 +912,24 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
 // per (row, query head) of merge item x: the wave reduces max and sum of the
 // split LSEs across its lanes, then accumulates the weighted partial rows.
 template <int D>
+__device__ __forceinline__ bool merge_item_ok(const MergeArgs &a, const int32_t *x)
+{
+    const int64_t seq_off = x[M_SEQ_OFF];
+    const int32_t r0 = x[M_R0], r1 = x[M_R1], ns = x[M_SPLITS], pb = x[M_PART_BASE];
+    const int rows = r1 - r0;
+    return rows >= 1 && rows <= a.tile && ns >= 1 && pb >= 0 &&
+           pb + (int64_t)ns * rows <= a.n_partial_rows && seq_off >= 0 && r0 >= 0 &&
+           seq_off + r1 <= a.total_tokens;
+}
+
+template <int D>
 __device__ __forceinline__ void merge_row(const MergeArgs &a, const int32_t *x, int rank,
                                           int head, int lane)
 {
     const int64_t seq_off = x[M_SEQ_OFF];
     const int32_t r0 = x[M_R0], r1 = x[M_R1], ns = x[M_SPLITS], pb = x[M_PART_BASE];
     const int rows = r1 - r0;
-    if (rows < 1 || rows > a.tile || rank >= rows || ns < 1 || pb < 0 ||
-        pb + (int64_t)ns * rows > a.n_partial_rows || seq_off < 0 || r0 < 0 ||
-        seq_off + r1 > a.total_tokens)
+    if (rank >= rows)
         return;
     const int row = r0 + rank;
 
@@ -980,15 +1017,24 @@ template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a)
 {
     const int32_t *sched = a.sched;
-    if (!header_ok(sched, a.total_tokens, a.n_items, a.kind) || sched[H_TILE] != a.tile)
+    const int64_t block = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    const int64_t n_blocks = (int64_t)gridDim.x * gridDim.y;
+    if (!header_ok(sched, a.total_tokens, a.n_items, a.kind) || sched[H_TILE] != a.tile) {
+        poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, block, n_blocks);
         return;
+    }
+    const int32_t *mi = sched + kHdrWords + (int64_t)a.n_items * kItemWords;
+    for (int m = blockIdx.y; m < a.n_merges; m += gridDim.y)
+        if (!merge_item_ok<D>(a, mi + (int64_t)m * kMergeWords)) {
+            poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, block, n_blocks);
+            return;
+        }
     const int lane = threadIdx.x & 63;
     const int w = (int)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (w >= a.tile * a.hq)
         return;
     const int head = w % a.hq;
     const int rank = w / a.hq;  // row within the merge item
-    const int32_t *mi = sched + kHdrWords + (int64_t)a.n_items * kItemWords;
     for (int m = blockIdx.y; m < a.n_merges; m += gridDim.y)
         merge_row<D>(a, mi + (int64_t)m * kMergeWords, rank, head, lane);
 }

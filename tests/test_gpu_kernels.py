@@ -169,6 +169,49 @@ def test_split_invariance():
                 o, lse, rows, range(8), label=f"splits={s} last rows")
 
 
+@pytest.mark.parametrize("kind", ["triangle", "causal", "blocksparse"])
+def test_corrupt_device_schedule_poisons_outputs(kind):
+    """A device schedule that does not match the launch is rejected by every
+    workgroup, which fills its slice of O and LSE with NaN (together every
+    element) instead of leaving stale values: the caller sees the failure.
+    Cases: a wrong magic word in the device header, and one malformed item
+    (rows past its sequence)."""
+    cu = [0, 700, 1024]
+    q, k, v = _cuda(*draw_qkv(cu, 8, 2, 128, 23))
+    if kind == "blocksparse":
+        ptr, idx = [0], []
+        for n in (700, 324):  # every q-tile keeps its diagonal and tile 0
+            for t in range(-(-n // 128)):
+                idx.extend(sorted({0, t}))
+                ptr.append(len(idx))
+        plan = binding.Plan("blocksparse", cu, 0, 1, 0, 128, 8, 128, device=q.device,
+                            blocks=(ptr, idx))
+    else:
+        plan = binding.Plan(kind, cu, 16, 128, 64, 128, 8, 128, device=q.device)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        o = torch.zeros(q.shape, dtype=out_dtype, device=q.device)
+        lse = torch.zeros((8, cu[-1]), dtype=torch.float32, device=q.device)
+        plan.run(q, k, v, o, lse, 0.1)
+        torch.cuda.synchronize()
+        assert not torch.isnan(o).any() and not torch.isnan(lse).any()
+        good = plan.sched.clone()
+        plan.sched[0] ^= 1  # magic word
+        plan.run(q, k, v, o, lse, 0.1)
+        torch.cuda.synchronize()
+        assert bool(torch.isnan(o).all()), (kind, out_dtype, "header")
+        assert bool(torch.isnan(lse).all()), (kind, out_dtype, "header")
+        plan.sched.copy_(good)
+        o.zero_()
+        lse.zero_()
+        item = binding.HDR_WORDS + binding.ITEM_WORDS * (plan.info.n_items - 1)
+        plan.sched[item + 3] = 1 << 20  # r1 (word 3) of the last item, past its sequence
+        plan.run(q, k, v, o, lse, 0.1)
+        torch.cuda.synchronize()
+        assert bool(torch.isnan(o).any()), (kind, out_dtype, "item")
+        plan.sched.copy_(good)
+        log(f"corrupt schedule {kind} {out_dtype}: outputs poisoned")
+
+
 def test_packing_invariance():
     cu = [0, 1000, 1000, 3100, 3300]
     q, k, v = _cuda(*draw_qkv(cu, 8, 2, 128, 6))
