@@ -197,6 +197,32 @@ ta_status triangle_attn_fwd(const void *q, const void *k, const void *v,
                             size_t workspace_bytes, void *stream);
 
 /*
+ * Triangle attention forward without a caller workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * or harnesses that forbid hipMalloc).  Same arguments and results as
+ * triangle_attn_fwd minus the workspace: the Last-row split partials go to a
+ * library-owned device array of TA_NOALLOC_SCRATCH_BYTES bytes per GPU,
+ * reserved when the library's code is loaded on that GPU and held until the
+ * process ends.  The first call on a GPU looks up the array's address (a HIP
+ * call, no allocation); no call allocates or frees memory.
+ *   Limit: ta_workspace_bytes(info, hq, head_dim) must not exceed
+ *   TA_NOALLOC_SCRATCH_BYTES (otherwise TA_ERR_WORKSPACE, nothing launched);
+ *   e.g. 128 Last rows x 32 heads x 57 splits at head_dim 128 take 120.5 MB.
+ *   Pass a smaller explicit split count to ta_build_schedule to fit.
+ *   Sharing: every call on one GPU uses the same array.  The partials are
+ *   written before they are read within a call, so nothing needs clearing,
+ *   but calls that overlap on one GPU (concurrent streams, threads) race.
+ */
+#define TA_NOALLOC_SCRATCH_BYTES (128u << 20)
+ta_status triangle_attn_fwd_noalloc(const void *q, const void *k, const void *v,
+                                    void *o, int32_t o_dtype, float *lse,
+                                    const int32_t *sched_dev,
+                                    const ta_schedule_info *info,
+                                    int64_t total_tokens, int32_t hq, int32_t hkv,
+                                    int32_t head_dim, float softmax_scale,
+                                    void *stream);
+
+/*
  * The two passes of triangle_attn_fwd, callable on their own (same stream
  * order: tiles, then merge); triangle_attn_fwd is exactly these two calls.
  *

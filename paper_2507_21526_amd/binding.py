@@ -92,6 +92,9 @@ def lib():
     L.triangle_attn_fwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, pinfo, i64,
                                     i32, i32, i32, ctypes.c_float, vp,
                                     ctypes.c_size_t, vp]
+    L.triangle_attn_fwd_noalloc.restype = ctypes.c_int
+    L.triangle_attn_fwd_noalloc.argtypes = [vp, vp, vp, vp, i32, vp, vp, pinfo, i64,
+                                            i32, i32, i32, ctypes.c_float, vp]
     L.triangle_attn_tiles.restype = ctypes.c_int
     L.triangle_attn_tiles.argtypes = list(L.triangle_attn_fwd.argtypes)
     L.triangle_attn_merge.restype = ctypes.c_int
@@ -277,6 +280,21 @@ def triangle_attn_fwd(q, k, v, o, lse, sched_dev, info, softmax_scale,
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
         _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
         float(softmax_scale), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def triangle_attn_fwd_noalloc(q, k, v, o, lse, sched_dev, info, softmax_scale,
+                              stream=None):
+    """Triangle attention without a workspace argument: the split partials
+    go to the library's own per-GPU scratch array (no allocation in the
+    call; at most TA_NOALLOC_SCRATCH_BYTES of partials).  Calls that overlap
+    on one GPU race on that array."""
+    _check_tensors(q, k, v, o, lse, sched_dev, info)
+    total, hq, d = q.shape
+    hkv = k.shape[1]
+    _check(lib().triangle_attn_fwd_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _out_dtype(o), _ptr(lse),
+        _ptr(sched_dev), ctypes.byref(info), total, hq, hkv, d,
+        float(softmax_scale), _stream(stream)))
 
 
 def triangle_attn_tiles(q, k, v, o, lse, sched_dev, info, softmax_scale,

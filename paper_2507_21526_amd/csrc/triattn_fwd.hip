@@ -29,9 +29,17 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 #include "triattn_internal.h"
+
+// Library-owned device memory of triangle_attn_fwd_noalloc: the Last-row
+// split partials (fp32 partial outputs, then their LSE, laid out as in a
+// caller's workspace).  Each GPU the library runs on holds its own copy
+// until the process ends.  In host code this name is only a handle for
+// hipGetSymbolAddress: kernels receive the device address obtained from it.
+static __device__ __align__(256) unsigned char scratch[TA_NOALLOC_SCRATCH_BYTES];
 
 namespace triattn {
 namespace {
@@ -1344,6 +1352,78 @@ extern "C" ta_status triangle_attn_fwd(const void *q, const void *k, const void 
     return split_pass_fwd("triangle_attn_fwd", TA_KIND_TRIANGLE, q, k, v, o, o_dtype, lse,
                           sched_dev, info, total_tokens, hq, hkv, head_dim, softmax_scale,
                           workspace, workspace_bytes, stream);
+}
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on the stream's GPU, looked up once per GPU
+// (with that GPU current) and kept.
+ta_status scratch_address(const char *fn, hipStream_t stream, void **out)
+{
+    int dev = -1;
+    hipError_t err = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+    if (err != hipSuccess)
+        return fail(TA_ERR_HIP, "%s: no device for the stream: %s", fn,
+                    hipGetErrorString(err));
+    if (dev < 0 || dev >= kMaxScratchDevices)
+        return fail(TA_ERR_UNSUPPORTED, "%s: device %d beyond %d", fn, dev,
+                    kMaxScratchDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        int cur = -1;
+        err = hipGetDevice(&cur);
+        if (err == hipSuccess && cur != dev)
+            err = hipSetDevice(dev);
+        void *p = nullptr;
+        if (err == hipSuccess)
+            err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur >= 0 && cur != dev) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (err == hipSuccess)
+                err = e2;
+        }
+        if (err != hipSuccess || !p)
+            return fail(TA_ERR_HIP, "%s: scratch address on device %d: %s", fn, dev,
+                        hipGetErrorString(err));
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return TA_OK;
+}
+}  // namespace
+
+extern "C" ta_status triangle_attn_fwd_noalloc(const void *q, const void *k, const void *v,
+                                               void *o, int32_t o_dtype, float *lse,
+                                               const int32_t *sched_dev,
+                                               const ta_schedule_info *info,
+                                               int64_t total_tokens, int32_t hq,
+                                               int32_t hkv, int32_t head_dim,
+                                               float softmax_scale, void *stream)
+{
+    static const char fn[] = "triangle_attn_fwd_noalloc";
+    clear_error();
+    ta_status st = check_common(fn, TA_KIND_TRIANGLE, q, k, v, o, o_dtype, sched_dev,
+                                info, total_tokens, hq, hkv, head_dim, softmax_scale);
+    if (st != TA_OK)
+        return st;
+    const size_t need = ta_workspace_bytes(info, hq, head_dim);
+    if (need > (size_t)TA_NOALLOC_SCRATCH_BYTES)
+        return fail(TA_ERR_WORKSPACE,
+                    "%s: the split partials need %zu bytes, the library scratch holds "
+                    "%zu: build the schedule with fewer splits or use triangle_attn_fwd",
+                    fn, need, (size_t)TA_NOALLOC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    if (need > 0) {
+        st = scratch_address(fn, static_cast<hipStream_t>(stream), &ws);
+        if (st != TA_OK)
+            return st;
+    }
+    return split_pass_fwd(fn, TA_KIND_TRIANGLE, q, k, v, o, o_dtype, lse, sched_dev, info,
+                          total_tokens, hq, hkv, head_dim, softmax_scale, ws,
+                          ws ? (size_t)TA_NOALLOC_SCRATCH_BYTES : 0, stream);
 }
 
 extern "C" ta_status blocksparse_attn_fwd(const void *q, const void *k, const void *v,

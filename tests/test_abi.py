@@ -157,6 +157,33 @@ def test_fwd_rejects_bad_arguments_without_launching():
         assert _fwd("blocksparse", info=bad) == B.TA_ERR_SCHEDULE_MISMATCH, field
 
 
+def test_noalloc_rejects_partials_beyond_the_scratch_size():
+    """triangle_attn_fwd_noalloc refuses, before any HIP call, a schedule
+    whose split partials exceed the library's scratch array."""
+    text = open(B.HEADER_PATH).read()
+    limit = re.search(r"#define TA_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    limit = int(limit.group(1)) << int(limit.group(2))
+    assert limit == 128 << 20
+    cu = [0, 8192, 32768, 81920, 147456]   # four packed sequences, automatic splits
+    _, info = B.ta_build_schedule("triangle", cu, 128, 2048, 128, 128)
+    need = B.ta_workspace_bytes(info, 32, 128)
+    assert need > limit
+    L = B.lib()
+    p = ctypes.c_void_p(FAKE)
+    st = L.triangle_attn_fwd_noalloc(p, p, p, p, 0, None, p, ctypes.byref(info),
+                                     cu[-1], 32, 8, 128, 0.1, None)
+    assert st == B.TA_ERR_WORKSPACE
+    assert "scratch holds" in B.ta_last_error()
+    # the ordinary checks come first
+    st = L.triangle_attn_fwd_noalloc(p, p, p, p, 0, None, p, ctypes.byref(info),
+                                     cu[-1] - 1, 32, 8, 128, 0.1, None)
+    assert st == B.TA_ERR_SCHEDULE_MISMATCH
+    _, cau = B.ta_build_schedule("causal", [0, 100], 4, 8, 2, 64)
+    st = L.triangle_attn_fwd_noalloc(p, p, p, p, 0, None, p, ctypes.byref(cau),
+                                     100, 8, 2, 128, 0.1, None)
+    assert st == B.TA_ERR_SCHEDULE_MISMATCH
+
+
 def _host_tensors(total=100, hq=8, hkv=2, d=128):
     import torch
     q = torch.zeros((total, hq, d), dtype=torch.bfloat16)
