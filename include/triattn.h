@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define TA_ABI_VERSION 2
+#define TA_ABI_VERSION 3
 #define TA_SCHEDULE_MAGIC 0x54524941
 #define TA_SCHEDULE_VERSION 2
 
@@ -95,6 +95,9 @@ typedef struct ta_schedule_info {
     int32_t n_partial_rows;   /* rows of split partials in the workspace */
     int32_t max_splits;       /* largest split count of a q-tile */
     int64_t kept_tiles_per_qhead; /* kept (q-tile, k-tile) pairs per head */
+    int32_t max_item_tiles;   /* most k-tiles of one work item (sizes the
+                                 launch of the attention pass) */
+    int32_t reserved;         /* 0 */
 } ta_schedule_info;
 
 /* Library interface version (TA_ABI_VERSION). */

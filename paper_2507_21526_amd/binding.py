@@ -52,6 +52,8 @@ class ScheduleInfo(ctypes.Structure):
         ("n_partial_rows", ctypes.c_int32),
         ("max_splits", ctypes.c_int32),
         ("kept_tiles_per_qhead", ctypes.c_int64),
+        ("max_item_tiles", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
     def as_dict(self):

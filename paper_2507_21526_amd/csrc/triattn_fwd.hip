@@ -27,8 +27,10 @@
 // list item reads its step keys from the list once, into an LDS table.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <mutex>
 #include <type_traits>
 
@@ -83,6 +85,11 @@ struct FwdArgs {
     int32_t subtiles;     // tile / R
     int32_t o_f32;
     float scale_log2;     // softmax scale * log2(e)
+    // multi-unit kernel: units = items x subtiles per kv head; workgroup
+    // (slot, head) runs units slot, slot + n_slots, ... (at most upw)
+    int32_t n_units;
+    int32_t n_slots;
+    int32_t upw;
 };
 
 struct MergeArgs {
@@ -915,6 +922,783 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         a.lse[(int64_t)head * a.total_tokens + seq_off + my_row] = row_lse;
 }
 
+// Multi-unit form of the tile kernel for workgroups of five to eight waves
+// (Q tiles in their own LDS region) over streaming and causal items.  A work
+// unit is one (item, row block) of the schedule for one kv head; workgroup w
+// owns kv head w % hkv and the units slot, slot + n_slots, slot + 2 n_slots,
+// ... (slot = w / hkv, at most upw of them), so the units in flight on the
+// chip at any time are neighbouring q-tiles of each kv head and share their
+// band K/V tiles in L2.  The units of a workgroup run as one continuous
+// pipeline of 64-key steps: the copies of K(j+1) and V(j) cross from one
+// unit into the next, each wave copies the next unit's Q rows into its LDS Q
+// tile while the current unit runs and reads them just before the next
+// unit's first matrix phase, and the finished unit's epilogue (normalise,
+// stage the bf16 rows in the now free Q tile, store whole rows) runs in the
+// softmax phase of the next unit's first step.  The per-unit costs of a
+// workgroup launch (schedule read, Q and first K tile from HBM, pipeline
+// fill and drain, the gap before the next workgroup) are paid once per
+// workgroup instead of once per unit.
+//
+// Before the pipeline starts, the workgroup turns its items into two LDS
+// tables: one record per unit (rows, sequence, output slot, first step) and
+// one word per pipeline step: the absolute token of the step's first key
+// (bits 6 and up; trimmed steps never start past their sequence) and the
+// number of its 64 keys that lie in the sequence, minus one (bits 0-5).  The
+// step loop then carries only the step index, the current unit's index, its
+// rows and the first step of the next unit.
+constexpr int kMaxUnits = 128;    // units per workgroup
+constexpr int kMaxSteps = 4096;   // pipeline steps per workgroup
+constexpr int64_t kMaxUnitsTokens = int64_t(1) << 26;  // tokens a step word can hold
+constexpr int kUnitWords = 12;    // unit record (see UnitField)
+enum UnitField {
+    U_START = 0, U_N, U_SEQ_OFF, U_SEQ_LEN, U_WR0, U_R1, U_PART, U_STREAM, U_A_LO, U_NA,
+    U_B_LO, U_PART_ROW0
+};
+
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32_t kind)
+{
+    constexpr int ROW_BYTES = 2 * D;
+    constexpr int CHUNKS = D / 8;
+    constexpr int TILE_BYTES = kStep * ROW_BYTES;
+    constexpr int STAGE_BYTES = 2 * TILE_BYTES;
+    constexpr int N_STAGES = 2;
+    constexpr int ROWS_PER_DMA = 1024 / ROW_BYTES;
+    constexpr int N_DMA = kStep / ROWS_PER_DMA;
+    constexpr int N_COPY_WAVES = NW - NW / 2;
+    constexpr int COPIES = (N_DMA + N_COPY_WAVES - 1) / N_COPY_WAVES;
+    constexpr int QK_STEPS = D / 16;
+    constexpr int D_BLOCKS = D / 32;
+    constexpr int MFMA_SLOTS = 2 * QK_STEPS + 4 * D_BLOCKS;
+    constexpr int COPY_STRIDE = MFMA_SLOTS / (2 * COPIES) > 0
+                                    ? MFMA_SLOTS / (2 * COPIES) : 1;
+    constexpr int QTILE_BYTES = 32 * ROW_BYTES;
+    constexpr int QREGION = N_STAGES * STAGE_BYTES;
+    static_assert(NW * QTILE_BYTES > STAGE_BYTES, "Q tiles have their own region");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[QREGION + NW * QTILE_BYTES];
+    __shared__ int32_t itab[kMaxUnits * kItemWords];  // the units' schedule items
+    // unit records, then one private slot per wave (units without steps)
+    __shared__ int32_t utab[(kMaxUnits + NW) * kUnitWords];
+    __shared__ int32_t stab[kMaxSteps];               // step words
+    typedef __attribute__((address_space(3))) int32_t lds_i32;
+    // Kernel arguments used only at unit boundaries (Q copies, epilogue),
+    // and the records of the current and next units, are held one word per
+    // lane in a vector register each and read with v_readlane where used:
+    // they take no scalar registers across the step loop and no memory
+    // round trip at a boundary.
+    struct BoundaryArgs {
+        const uint16_t *q;
+        void *o;
+        float *lse, *part_o, *part_lse;
+        int64_t total_tokens;
+        int32_t hq, o_f32;
+    };
+    constexpr int kArgWords = (int)(sizeof(BoundaryArgs) / 4);
+    static_assert(kArgWords <= 64 && kUnitWords <= 64, "one word per lane");
+    __shared__ BoundaryArgs bargs;
+
+    const int32_t *sched = a.sched;
+    const int g = blockIdx.x % a.hkv;
+    const int slot = blockIdx.x / a.hkv;
+    const int n_my = min(a.upw, (a.n_units - slot + a.n_slots - 1) / a.n_slots);
+    if (slot >= a.n_slots || n_my <= 0)
+        return;
+    if (!header_ok(sched, a.total_tokens, a.n_items, kind) || a.list_words != 0 ||
+        n_my > kMaxUnits) {
+        poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x, gridDim.x);
+        return;
+    }
+    for (int t = threadIdx.x; t < n_my * kItemWords; t += NW * 64) {
+        const int u = slot + (t / kItemWords) * a.n_slots;
+        const int item = u / a.subtiles;
+        itab[t] = sched[kHdrWords + (int64_t)item * kItemWords + t % kItemWords];
+    }
+    if (threadIdx.x == 0)
+        bargs = BoundaryArgs{a.q, a.o, a.lse, a.part_o, a.part_lse, a.total_tokens, a.hq,
+                             a.o_f32};
+    __syncthreads();
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = lane >> 5;
+    const int col = lane & 31;
+    // The lane index as the compiler cannot see it: per-lane addresses of the
+    // rarely run unit-boundary code (Q copies, epilogue) are derived from it,
+    // so they are recomputed there instead of being hoisted out of the step
+    // loop into registers that would stay live across every step.
+    auto opaque_lane = [&]() TA_INLINE -> int {
+        int x = lane;
+        asm volatile("" : "+v"(x));
+        return x;
+    };
+    const int args_v = lane < kArgWords ? ((lds_i32 *)&bargs)[lane] : 0;
+    auto args = [&]() TA_INLINE -> BoundaryArgs {
+        int av = args_v;
+        asm volatile("" : "+v"(av));  // read here, not hoisted into scalars
+        uint32_t v[kArgWords];
+#pragma unroll
+        for (int i = 0; i < kArgWords; ++i)
+            v[i] = (uint32_t)__builtin_amdgcn_readlane(av, i);
+        return __builtin_bit_cast(BoundaryArgs, v);
+    };
+    const int waves_per_head = a.rows_per_wg / 32;
+    const int head = g * a.group + wave / waves_per_head;
+    const int wave_row = (wave % waves_per_head) * 32;  // first row of the wave in a unit
+    const float c = a.scale_log2;
+    const int tps = a.tile / kStep;
+    // unit record k, one word per lane; field f of it
+    auto rec_of = [&](int ku) TA_INLINE -> int {
+        return lane < kUnitWords
+                   ? ((lds_i32 *)utab)[__builtin_amdgcn_readfirstlane(ku) * kUnitWords + lane]
+                   : 0;
+    };
+    auto fld = [](int rv, int f) TA_INLINE -> int { return __builtin_amdgcn_readlane(rv, f); };
+
+    const uint32_t smem_addr =
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
+    const uint32_t qtile_lds = smem_addr + QREGION + wave * QTILE_BYTES;
+    // Copy the wave's 32 Q rows of unit ku into its LDS Q tile (rows past the
+    // unit's rows repeat its last row).
+    auto copy_q = [&](int rv) TA_INLINE {
+        const int r1 = fld(rv, U_R1);
+        const int row_base = fld(rv, U_WR0) + wave_row;
+        const int q_row0 = min(row_base, r1 - 1);
+        const int q_tok = fld(rv, U_SEQ_OFF) + q_row0;
+        const BoundaryArgs ka = args();
+        const int hq = ka.hq;
+        const uint16_t *qb = ka.q + ((int64_t)q_tok * hq + head) * (int64_t)D;
+        const uint32_t q_pitch = (uint32_t)(hq * ROW_BYTES);
+        const int ln = opaque_lane();
+#pragma unroll
+        for (int i = 0; i < QTILE_BYTES / 1024; ++i) {
+            const int row = i * (1024 / ROW_BYTES) + ln / CHUNKS;
+            const int rr = min(row_base + row, r1 - 1) - q_row0;
+            const uint32_t off = __umul24((uint32_t)rr, q_pitch) +
+                                 (uint32_t)(((ln % CHUNKS) ^ kswz<D>(row)) << 4);
+            copy_to_lds16(qb, off, qtile_lds + i * 1024);
+        }
+    };
+    bf16x8 qf[QK_STEPS];
+    auto read_q = [&]() TA_INLINE {
+        const int ln = opaque_lane();
+        const int cl = ln & 31, hf = ln >> 5;
+        const unsigned char *qt = smem + QREGION + wave * QTILE_BYTES + cl * ROW_BYTES;
+#pragma unroll
+        for (int s = 0; s < QK_STEPS; ++s)
+            qf[s] = *reinterpret_cast<const bf16x8 *>(qt + (((2 * s + hf) ^ kswz<D>(cl)) << 4));
+    };
+
+    f32x16 oacc[D_BLOCKS];
+#pragma unroll
+    for (int b = 0; b < D_BLOCKS; ++b)
+        oacc[b] = f32x16{};
+
+    // Epilogue of unit ku: O (or its normalised fp32 partial) and LSE of the
+    // wave's rows, from oacc and the unit's l / m.  bf16 rows are staged in
+    // the wave's Q tile (free: the next unit's Q has been read) and stored
+    // whole.  Addresses: a uniform base at the wave's first row plus a
+    // 32-bit per-lane offset.
+    auto epilogue = [&](int rv, float l_sum, float m_row) TA_INLINE {
+        const int r1 = fld(rv, U_R1);
+        const int row_base = fld(rv, U_WR0) + wave_row;
+        if (row_base >= r1)
+            return;  // a ragged unit: this wave has no rows
+        // partial row of sequence row r: part + r (a unit without partials
+        // has U_PART = -1)
+        const bool has_part = fld(rv, U_PART) >= 0;
+        const int part = has_part ? fld(rv, U_PART_ROW0) : 0;
+        const int64_t row_tok = (int64_t)fld(rv, U_SEQ_OFF) + row_base;
+        const int ln = opaque_lane();
+        const int col = ln & 31, half = ln >> 5;
+        const bool row_valid = row_base + col < r1;
+        const float l_tot = pair_sum(l_sum);
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        const float row_lse = l_tot > 0.f ? (m_row + __log2f(l_tot)) * kLn2 : -INFINITY;
+        const BoundaryArgs ka = args();
+        const int hq = ka.hq;
+        const uint32_t hd = (uint32_t)(hq * D);  // elements per token
+        float *lse_row = nullptr;
+        if (has_part)
+            lse_row = ka.part_lse + ((int64_t)(part + row_base) * hq + head);
+        else if (ka.lse)
+            lse_row = ka.lse + (int64_t)head * ka.total_tokens + row_tok;
+        const uint32_t lse_step = has_part ? (uint32_t)hq : 1u;
+        if (!has_part && !ka.o_f32) {
+            constexpr int ROWB = D * 2;
+            constexpr int CHK = ROWB / 16;
+            static_assert(32 * ROWB == QTILE_BYTES, "an output tile fills a Q tile");
+            unsigned char *tile = smem + QREGION + wave * QTILE_BYTES;
+            auto oswz = [](int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
+#pragma unroll
+            for (int b = 0; b < D_BLOCKS; ++b)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    f32x4 t;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        t[e] = oacc[b][4 * j + e] * inv;
+                    const int pc = (4 * b + j) ^ oswz(col);
+                    *reinterpret_cast<bf16x4 *>(tile + col * ROWB + pc * 16 + half * 8) =
+                        __builtin_convertvector(t, bf16x4);
+                }
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+            asm volatile("" ::: "memory");
+            char *obase = reinterpret_cast<char *>(
+                reinterpret_cast<__bf16 *>(ka.o) + (row_tok * hq + head) * (int64_t)D);
+            constexpr int NCH = 32 * CHK / 64;  // 16-byte pieces per lane
+            u32x4 val[NCH];
+#pragma unroll
+            for (int kk = 0; kk < NCH; ++kk) {  // every LDS read first, then the stores
+                const int rr = ln / CHK + kk * (64 / CHK);
+                const int cc = ln % CHK;
+                val[kk] = *reinterpret_cast<const u32x4 *>(tile + rr * ROWB +
+                                                           ((cc ^ oswz(rr)) << 4));
+            }
+#pragma unroll
+            for (int kk = 0; kk < NCH; ++kk) {
+                const int rr = ln / CHK + kk * (64 / CHK);
+                const int cc = ln % CHK;
+                if (row_base + rr < r1)
+                    *reinterpret_cast<u32x4 *>(obase + (uint64_t)((uint32_t)rr * hd * 2u +
+                                                                  (uint32_t)cc * 16u)) = val[kk];
+            }
+            // the staged tile is read before the Q tile is reused
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            asm volatile("" ::: "memory");
+        } else if (row_valid) {
+            float *po = has_part
+                            ? ka.part_o + ((int64_t)(part + row_base) * hq + head) * D
+                            : reinterpret_cast<float *>(ka.o) + (row_tok * hq + head) * D;
+            const uint32_t lane_off = (uint32_t)col * hd + 4u * (uint32_t)half;
+#pragma unroll
+            for (int b = 0; b < D_BLOCKS; ++b)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    f32x4 t;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        t[e] = oacc[b][4 * j + e] * inv;
+                    *reinterpret_cast<f32x4 *>(po + (uint64_t)(lane_off + b * 32 + 8 * j)) = t;
+                }
+        }
+        if (lse_row && half == 0 && row_valid)
+            lse_row[(uint64_t)((uint32_t)col * lse_step)] = row_lse;
+    };
+
+    // Pass 1 (every wave, scalar): validate each item (a malformed one
+    // poisons the outputs before any work), pick the workgroup's rows, trim
+    // the key runs to them (as the single-unit kernel does) and append a
+    // record for every unit with steps.  Units without rows here are
+    // dropped; a unit with rows but no steps (an empty split of a Last
+    // q-tile) is written at once (zero partials, LSE -inf).
+    int n_run = 0, n_total = 0;
+    for (int k = 0; k < n_my; ++k) {
+        lds_i32 *w = (lds_i32 *)itab + k * kItemWords;
+        const int seq_off = __builtin_amdgcn_readfirstlane(w[I_SEQ_OFF]);
+        const int seq_len = __builtin_amdgcn_readfirstlane(w[I_SEQ_LEN]);
+        const int r0 = __builtin_amdgcn_readfirstlane(w[I_R0]);
+        const int r1 = __builtin_amdgcn_readfirstlane(w[I_R1]);
+        const int ka0 = __builtin_amdgcn_readfirstlane(w[I_KA0]);
+        const int ka1 = __builtin_amdgcn_readfirstlane(w[I_KA1]);
+        const int kb0 = __builtin_amdgcn_readfirstlane(w[I_KB0]);
+        const int kb1 = __builtin_amdgcn_readfirstlane(w[I_KB1]);
+        const int mode = __builtin_amdgcn_readfirstlane(w[I_MODE]);
+        const int part_base = __builtin_amdgcn_readfirstlane(w[I_PART_BASE]);
+        if (seq_off < 0 || seq_len < 0 || (int64_t)seq_off + seq_len > a.total_tokens ||
+            r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || ka1 < ka0 || kb0 < 0 ||
+            kb1 < kb0 || (mode != kModeStreaming && mode != kModeCausal) ||
+            (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows)) {
+            poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x,
+                           gridDim.x);
+            return;
+        }
+        const int sub = (slot + k * a.n_slots) % a.subtiles;
+        const int wr0 = r0 + sub * a.rows_per_wg;
+        if (wr0 >= r1)
+            continue;
+        const bool stream = mode == kModeStreaming;
+        int a_lo = ka0 * tps, a_hi = ka1 * tps, b_lo = kb0 * tps, b_hi = kb1 * tps;
+        const int wr_last = min(wr0 + a.rows_per_wg, r1) - 1;
+        if (stream) {
+            const int first = wr0 - a.window + 1;
+            const int fs = first > 0 ? first / kStep : 0;
+            if (b_hi > b_lo)
+                b_lo = min(max(b_lo, fs), b_hi);
+            else if (a.sink == 0)
+                a_lo = min(max(a_lo, fs), a_hi);
+        }
+        const int ls = wr_last / kStep + 1;
+        if (b_hi > b_lo)
+            b_hi = max(min(b_hi, ls), b_lo);
+        else
+            a_hi = max(min(a_hi, ls), a_lo);
+        const int na = a_hi - a_lo;
+        const int n = na + (b_hi - b_lo);
+        const int rec[kUnitWords] = {n_total, n, seq_off, seq_len, wr0, r1, part_base,
+                                     stream ? 1 : 0, a_lo, na, b_lo, part_base - r0};
+        if (n > 0 && (n_total + n > kMaxSteps || n_run >= kMaxUnits)) {
+            poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x,
+                           gridDim.x);
+            return;
+        }
+        // every wave writes the same record words (one word per lane); a
+        // unit without steps goes to the wave's private slot, is written
+        // through the epilogue (oacc is zero) and dropped
+        const int rslot = n == 0 ? kMaxUnits + wave : n_run;
+        if (lane < kUnitWords) {
+            int v = rec[0];
+#pragma unroll
+            for (int f = 1; f < kUnitWords; ++f)
+                v = lane == f ? rec[f] : v;
+            utab[rslot * kUnitWords + lane] = v;
+        }
+        if (n == 0) {
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            epilogue(rec_of(rslot), 0.f, -INFINITY);
+            continue;
+        }
+        ++n_run;
+        n_total += n;
+    }
+    __syncthreads();  // unit records written (the same words by every wave)
+    if (n_total == 0)
+        return;
+    // Pass 2: wave w fills the step records of units w, w + NW, ...
+    for (int ku = wave; ku < n_run; ku += NW) {
+        const int rv = rec_of(ku);
+        const int start = fld(rv, U_START), n = fld(rv, U_N);
+        const int seq_off = fld(rv, U_SEQ_OFF), key_max = fld(rv, U_SEQ_LEN) - 1;
+        const int a_lo = fld(rv, U_A_LO), na = fld(rv, U_NA), b_lo = fld(rv, U_B_LO);
+        for (int s = lane; s < n; s += 64) {
+            const int key0 = s < na ? (a_lo + s) * kStep : (b_lo + (s - na)) * kStep;
+            stab[start + s] = ((seq_off + key0) << 6) | min(key_max - key0, kStep - 1);
+        }
+    }
+    __syncthreads();
+
+    // K/V tile copies (as the single-unit kernel) from a step record: the
+    // absolute token of the tile's first row and its valid rows - 1; rows
+    // past the sequence end read its last row (they lie beyond every row of
+    // the unit, so the causal mask removes them).
+    const uint16_t *kbase = a.k + (int64_t)g * D;
+    const uint16_t *vbase = a.v + (int64_t)g * D;
+    const int tok_stride = a.hkv * D;
+    const bool copy_wave = wave < N_COPY_WAVES;
+    const int dma_row_in = lane / CHUNKS;
+    const int dma_pc = lane % CHUNKS;
+    const uint32_t kx0 = (uint32_t)((dma_pc ^ kswz<D>(dma_row_in)) << 4);
+    const uint32_t vx0 = (uint32_t)((dma_pc ^ vswz<D>(dma_row_in)) << 4);
+    const uint32_t row_stride_bytes = 2u * (uint32_t)tok_stride;
+    const uint32_t dma_off0 =
+        __umul24((uint32_t)(wave * ROWS_PER_DMA + dma_row_in), row_stride_bytes);
+    const uint32_t dma_off_step = (uint32_t)(N_COPY_WAVES * ROWS_PER_DMA) * row_stride_bytes;
+    constexpr bool XR_PER_WAVE = D == 128 ? N_COPY_WAVES % 4 == 0 : N_COPY_WAVES % 2 == 0;
+    struct TileCopy {
+        const uint16_t *base;
+        uint32_t lds;
+        uint32_t lim;
+    };
+    auto srec = [&](int j) TA_INLINE -> uint32_t {
+        return (uint32_t)__builtin_amdgcn_readfirstlane(
+            ((lds_i32 *)stab)[__builtin_amdgcn_readfirstlane(j)]);
+    };
+    auto plan_copy = [&](const uint16_t *src, uint32_t w, int buf, bool is_v) TA_INLINE -> TileCopy {
+        w = (uint32_t)__builtin_amdgcn_readfirstlane(w);  // uniform (a step word)
+        TileCopy t;
+        t.base = src + (int64_t)(w >> 6) * tok_stride;
+        t.lim = (w & (kStep - 1)) * row_stride_bytes;
+        t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0) + wave * 1024;
+        // opaque: each copy adds its own offset (one scalar add) instead of
+        // every copy address of both stages being held in its own register
+        asm volatile("" : "+s"(t.lds));
+        return t;
+    };
+    auto issue_copy = [&](const TileCopy &t, int i, bool is_v) TA_INLINE {
+        const int m = wave + i * N_COPY_WAVES;
+        if constexpr (N_DMA % N_COPY_WAVES != 0) {
+            if (m >= N_DMA)
+                return;
+        }
+        const uint32_t xr = is_v ? vx0 : (kx0 ^ (uint32_t)(kswz<D>(m * ROWS_PER_DMA) << 4));
+        uint32_t off;
+        if constexpr (XR_PER_WAVE)
+            off = min(dma_off0 + (uint32_t)i * dma_off_step + xr, t.lim + xr);
+        else
+            off = min(dma_off0 + (uint32_t)i * dma_off_step, t.lim) + xr;
+        copy_to_lds16(t.base, off, t.lds + i * (N_COPY_WAVES * 1024));
+    };
+    TileCopy cp_k{}, cp_v{};
+    auto issue_slot = [&](int cidx) TA_INLINE {
+        if (cidx < COPIES)
+            issue_copy(cp_k, cidx, false);
+        else
+            issue_copy(cp_v, cidx - COPIES, true);
+    };
+    auto copy_hook = [&](int mslot) TA_INLINE {
+        if (mslot % COPY_STRIDE == COPY_STRIDE - 1 && mslot / COPY_STRIDE < 2 * COPIES)
+            issue_slot(mslot / COPY_STRIDE);
+    };
+    auto no_hook = [](int) {};
+
+    const int krow0 = perm_row(col);
+    uint32_t koff[QK_STEPS];
+#pragma unroll
+    for (int s = 0; s < QK_STEPS; ++s)
+        koff[s] = (uint32_t)(krow0 * ROW_BYTES + (((2 * s + half) ^ kswz<D>(krow0)) << 4));
+    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) TA_INLINE {
+        const unsigned char *kt = smem + buf * STAGE_BYTES;
+        sacc[0] = f32x16{};
+        sacc[1] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < QK_STEPS; ++s) {
+            const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(kt + koff[s]);
+            const bf16x8 a1 =
+                *reinterpret_cast<const bf16x8 *>(kt + koff[s] + 32 * ROW_BYTES);
+            sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], sacc[0], 0, 0, 0);
+            hook(2 * s);
+            sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], sacc[1], 0, 0, 0);
+            hook(2 * s + 1);
+        }
+        constexpr int n = 2 * QK_STEPS, ahead = 6;
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
+#pragma unroll
+        for (int i = 0; i < n - ahead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
+    };
+    const int vrow0 = 8 * half + ((lane & 15) >> 2);
+    const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    uint32_t voff[D_BLOCKS];
+#pragma unroll
+    for (int b = 0; b < D_BLOCKS; ++b) {
+        const int d = 32 * b + tr_d;
+        voff[b] = (uint32_t)(vrow0 * ROW_BYTES + (((d >> 3) ^ vswz<D>(vrow0)) << 4) +
+                             (d & 7) * 2);
+    }
+    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) TA_INLINE {
+        const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+                for (int b = 0; b < D_BLOCKS; ++b) {
+                    s16x4 part[2];
+#pragma unroll
+                    for (int i2 = 0; i2 < 2; ++i2)
+                        part[i2] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4 *)(vt + voff[b] +
+                                          (kb * 32 + s2 * 16 + 4 * i2) * ROW_BYTES));
+                    const bf16x8 af = __builtin_bit_cast(
+                        bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5,
+                                                        6, 7));
+                    oacc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pf[kb][s2],
+                                                                     oacc[b], 0, 0, 0);
+                    hook(2 * QK_STEPS + (kb * 2 + s2) * D_BLOCKS + b);
+                }
+        constexpr int n = 4 * D_BLOCKS, ahead = 4;
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * ahead, 0);
+#pragma unroll
+        for (int i = 0; i < n - ahead; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
+    };
+
+    // The current unit, as the mask needs it (uniform).
+    int ku = 0;                        // current unit
+    int next_start = 0;                // first step of unit ku + 1 (n_total: none)
+    int cur_row_base = 0, cur_row_hi = 0, cur_stream = 0, cur_seq_off = 0;
+    int rec_cur = rec_of(0);                           // current unit
+    int rec_nxt = n_run > 1 ? rec_of(1) : rec_cur;     // the next one
+    auto enter_unit = [&](int k) TA_INLINE {
+        ku = k;
+        next_start = k + 1 < n_run ? fld(rec_nxt, U_START) : n_total;
+        cur_seq_off = fld(rec_cur, U_SEQ_OFF);
+        const int r1 = fld(rec_cur, U_R1);
+        cur_row_base = fld(rec_cur, U_WR0) + wave_row;
+        cur_row_hi = min(r1 - 1, cur_row_base + 31);
+        cur_stream = fld(rec_cur, U_STREAM);
+    };
+
+    // Masks of one step.  A step can cross the diagonal (causal test), the
+    // window edge of streaming rows (window test, the sink excepted) or
+    // both; each case gets its own branch-free selects.  The window tests
+    // use the sign of a difference as the select mask (a vector operation
+    // per element, no lane mask in scalar registers: batches of compares
+    // into lane masks would take dozens of scalar registers).
+    auto keep_if = [](float sc, int m) TA_INLINE -> float {
+        // m = -1: keep the score, m = 0: -inf
+        return __builtin_bit_cast(float, (__builtin_bit_cast(uint32_t, sc) & (uint32_t)m) |
+                                              (0xff800000u & ~(uint32_t)m));
+    };
+    auto mask_step = [&](int key0, f32x16 (&sacc)[2]) TA_INLINE {
+        const int my_row = cur_row_base + col;
+        const bool need_causal = key0 + kStep - 1 > cur_row_base;
+        const bool need_window = cur_stream && key0 + kStep - 1 >= a.sink &&
+                                 cur_row_hi - key0 >= a.window;
+        const int lim = my_row - key0 - 8 * half;  // key offset <= lim: causal
+        if (!need_window) {
+            if (need_causal) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int off = kb * 32 + key_of_reg(v, 0);
+                        sacc[kb][v] = off <= lim ? sacc[kb][v] : -INFINITY;
+                    }
+            }
+            return;
+        }
+        const int win_lim = lim - a.window;             // offset > win_lim: in the window
+        const int sink_lim = a.sink - key0 - 8 * half;  // offset < sink_lim: a sink key
+        if (!need_causal && key0 >= a.sink) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int off = kb * 32 + key_of_reg(v, 0);
+                    sacc[kb][v] = keep_if(sacc[kb][v], (win_lim - off) >> 31);
+                }
+            return;
+        }
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int off = kb * 32 + key_of_reg(v, 0);
+                const int m = ~((lim - off) >> 31) & (((off - sink_lim) >> 31) | ((win_lim - off) >> 31));
+                sacc[kb][v] = keep_if(sacc[kb][v], m);
+            }
+    };
+    auto step_needs_mask = [&](int key0) TA_INLINE -> bool {
+        return (key0 + kStep - 1 > cur_row_base) ||
+               (cur_stream && key0 + kStep - 1 >= a.sink && cur_row_hi - key0 >= a.window);
+    };
+
+    float m_ref = -INFINITY;
+    float l_run = 0.f;
+    bool fresh = true;  // the unit's first softmax: no reference maximum on any lane
+    auto softmax = [&](f32x16 (&sacc)[2], bf16x8 (&pf)[2][2]) TA_INLINE {
+        auto exp_step = [&](float m_use) TA_INLINE -> float {
+            float psum = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int s2 = 0; s2 < 2; ++s2) {
+                    f32x8 t;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        t[e] = __builtin_amdgcn_exp2f(
+                            __builtin_fmaf(sacc[kb][8 * s2 + e], c, -m_use));
+                        psum += t[e];
+                    }
+                    pf[kb][s2] = __builtin_convertvector(t, bf16x8);
+                }
+            return psum;
+        };
+        // The first step of a unit has no reference on any lane: it goes
+        // straight to the re-base (its first pass would be discarded).
+        float psum = INFINITY;
+        if (!fresh)
+            psum = exp_step(m_ref == -INFINITY ? 0.f : m_ref);
+        fresh = false;
+        const bool bad = !(psum <= kRescaleBound) || m_ref == -INFINITY;
+        if (__builtin_amdgcn_ballot_w64(bad) != 0) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    mx = fmaxf(mx, sacc[kb][v]);
+            mx = pair_max(mx);
+            const float m_new = fmaxf(m_ref, mx * c);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+            const float alpha = __builtin_amdgcn_exp2f(m_ref - m_use);
+            l_run *= alpha;
+#pragma unroll
+            for (int b = 0; b < D_BLOCKS; ++b)
+                oacc[b] *= alpha;
+            m_ref = m_new;
+            psum = exp_step(m_use);
+        }
+        l_run += psum;
+    };
+
+    // Step words, read one phase ahead of their use: wk and wv for the
+    // copies of K(j+1) and V(j) in the matrix phase of step j (steps past the
+    // last one copy a repeat of the last K tile into parts of the stage
+    // nobody reads), wx for the mask of the next softmax phase.
+    uint32_t wk = 0, wv = 0, wx = 0;
+    auto plan_step_copies = [&](auto stage) TA_INLINE {
+        const int nbuf = 1 - (int)stage;
+        cp_k = plan_copy(kbase, wk, nbuf, false);
+        cp_v = plan_copy(vbase, wv, nbuf, true);
+    };
+
+    const int n_group1 = NW / 2;
+    const int group = wave >= NW - n_group1 ? 1 : 0;
+    f32x16 s_acc[2];
+    bf16x8 p_acc[2][2];
+    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook) TA_INLINE {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+        __builtin_amdgcn_sched_barrier(0);
+        const int buf = stage;
+        if (has_qk)
+            qk(buf, s_acc, hook);
+        if (has_pv)
+            pv(buf, p_acc, hook);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto do_x = [&]() TA_INLINE {
+        const int key0 = (int)(__builtin_amdgcn_readfirstlane(wx) >> 6) - cur_seq_off;
+        if (step_needs_mask(key0))
+            mask_step(key0, s_acc);
+        softmax(s_acc, p_acc);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2)
+                fence_regs(p_acc[kb][s2]);
+        fence_regs(l_run);
+        fence_regs(m_ref);
+    };
+    auto end_phase = [&](bool wait_copies) TA_INLINE {
+        __builtin_amdgcn_sched_barrier(0);
+        if (wait_copies)
+            wait_vmcnt(0);
+        barrier_no_fence();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // Unit boundary, in the softmax phase of the new unit's first step
+    // (after the matrix phase that finished the old unit's PV): write the old
+    // unit, make the new one current, start copying the Q rows of the one
+    // after it.
+    auto boundary = [&]() TA_INLINE {
+        epilogue(rec_cur, l_run, m_ref);
+#pragma unroll
+        for (int b = 0; b < D_BLOCKS; ++b)
+            oacc[b] = f32x16{};
+        m_ref = -INFINITY;
+        l_run = 0.f;
+        fresh = true;
+        rec_cur = rec_nxt;
+        rec_nxt = ku + 2 < n_run ? rec_of(ku + 2) : rec_cur;
+        enter_unit(ku + 1);
+        if (ku + 1 < n_run)
+            copy_q(rec_nxt);
+    };
+    using Stage0 = std::integral_constant<int, 0>;
+    using Stage1 = std::integral_constant<int, 1>;
+
+    // Prologue: every wave copies its Q rows of the first unit, the copy
+    // waves copy K(0) into stage 0; after the barrier each wave reads its Q
+    // and starts copying the next unit's Q rows.
+    enter_unit(0);
+    copy_q(rec_cur);
+    if (copy_wave) {
+        cp_k = plan_copy(kbase, srec(0), 0, false);
+#pragma unroll
+        for (int cidx = 0; cidx < COPIES; ++cidx)
+            issue_slot(cidx);
+    }
+    end_phase(true);
+    read_q();
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // Q read before its tile is refilled
+    if (n_run > 1)
+        copy_q(rec_nxt);
+    if (group == 0) {
+        wk = srec(min(1, n_total - 1));
+        wv = srec(0);
+        plan_step_copies(Stage0{});
+        do_m(Stage0{}, true, false, copy_hook);
+#pragma unroll
+        for (int cidx = 0; cidx < 2 * COPIES; ++cidx)
+            if (cidx * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
+                issue_slot(cidx);
+        end_phase(false);
+        // softmax of step j (its word is wv), then the words of step j + 1
+        auto x_phase = [&](int j) TA_INLINE {
+            const int nv = ((lds_i32 *)stab)[min(j + 1, n_total - 1)];
+            const int nk = ((lds_i32 *)stab)[min(j + 2, n_total - 1)];
+            wx = wv;
+            do_x();
+            wv = (uint32_t)__builtin_amdgcn_readfirstlane(nv);
+            wk = (uint32_t)__builtin_amdgcn_readfirstlane(nk);
+        };
+        x_phase(0);
+        end_phase(true);
+        // the Q copy of the next unit has landed at every unit start: the
+        // last phase of each step waits for this wave's copies
+        auto step = [&](int j, auto stage) TA_INLINE {
+            const bool bnd = j == next_start;
+            if (bnd)
+                read_q();
+            plan_step_copies(stage);
+            do_m(stage, true, true, copy_hook);
+            end_phase(false);
+            if (bnd)
+                boundary();
+            x_phase(j);
+            end_phase(true);
+        };
+        int j = 1;
+        for (; j + 1 < n_total; j += 2) {
+            step(j, Stage1{});
+            step(j + 1, Stage0{});
+        }
+        if (j < n_total)
+            step(j++, Stage1{});
+        do_m(j & 1, false, true, no_hook);
+        end_phase(false);
+        end_phase(false);
+    } else {
+        end_phase(false);
+        int nx = ((lds_i32 *)stab)[0];
+        do_m(Stage0{}, true, false, no_hook);
+        end_phase(false);
+        // the word of step j - 1 was read during the matrix phase before
+        auto step = [&](int j, auto stage) TA_INLINE {
+            if (j - 1 == next_start)
+                boundary();
+            wx = (uint32_t)__builtin_amdgcn_readfirstlane(nx);
+            do_x();
+            end_phase(false);
+            if (j == next_start) {
+                wait_vmcnt(0);  // the next unit's Q rows have landed
+                read_q();
+            }
+            nx = ((lds_i32 *)stab)[j];
+            do_m(stage, true, true, no_hook);
+            end_phase(false);
+        };
+        int j = 1;
+        for (; j + 1 < n_total; j += 2) {
+            step(j, Stage1{});
+            step(j + 1, Stage0{});
+        }
+        if (j < n_total)
+            step(j++, Stage1{});
+        if (j - 1 == next_start)
+            boundary();
+        wx = (uint32_t)__builtin_amdgcn_readfirstlane(nx);
+        do_x();
+        end_phase(false);
+        do_m(j & 1, false, true, no_hook);
+        end_phase(false);
+    }
+    epilogue(rec_cur, l_run, m_ref);
+}
+
 // LSE-weighted merge of the split partials of one q-tile (the Last rows of
 // Triangle attention, or a block-sparse q-tile cut into chunks).  One wave
 // per (row, query head) of merge item x: the wave reduces max and sum of the
@@ -1167,17 +1951,85 @@ FwdArgs make_args(const void *q, const void *k, const void *v, void *o,
     a.subtiles = info->tile / R;
     a.o_f32 = o_dtype == TA_OUT_F32;
     a.scale_log2 = scale * kLog2e;
+    a.n_units = 0;
+    a.n_slots = 0;
+    a.upw = 1;
     return a;
 }
 
-ta_status launch_tiles(int kind, const FwdArgs &a, int32_t head_dim, hipStream_t stream)
+template <int D>
+hipError_t launch_units(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_t s)
 {
-    if (a.n_items <= 0)
+    switch (nw) {
+    case 5: hipLaunchKernelGGL((attn_units_kernel<D, 5>), grid, dim3(320), 0, s, a, kind); break;
+    case 6: hipLaunchKernelGGL((attn_units_kernel<D, 6>), grid, dim3(384), 0, s, a, kind); break;
+    case 7: hipLaunchKernelGGL((attn_units_kernel<D, 7>), grid, dim3(448), 0, s, a, kind); break;
+    case 8: hipLaunchKernelGGL((attn_units_kernel<D, 8>), grid, dim3(512), 0, s, a, kind); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// Units per workgroup of the multi-unit kernel for a Triangle pass, or 1
+// for the single-unit kernel.  A unit boundary costs about as much as the
+// per-workgroup costs it removes (measured: about 10 K cycles, the
+// epilogue's normalisation, staging and stores beside the other group's
+// MFMAs), and the pass runs at a power-limited clock, so the multi-unit
+// kernel pays off only for short units (the paper's sink 8 / window 512
+// shape: 12 steps, 5 % faster; 36-step units at window 2048: 1-3 % slower).
+// For units of at most kShortUnitSteps steps: one workgroup per CU (256 CUs
+// over the kv heads) when its units' steps fit the LDS step table,
+// otherwise the fewest rounds of such workgroups whose units fit.  The
+// environment variable TRIATTN_UNITS_PER_WG, read at every launch,
+// overrides the count (1: the single-unit kernel) within the table limits:
+// for tests and tuning.
+constexpr int64_t kShortUnitSteps = 16;
+int units_per_wg(const FwdArgs &a, int kind, int nw, int64_t units, int32_t max_item_tiles)
+{
+    if (kind != TA_KIND_TRIANGLE || nw < 5 || units > INT32_MAX ||
+        a.total_tokens >= kMaxUnitsTokens || max_item_tiles < 1)
+        return 1;
+    const int64_t unit_steps = (int64_t)max_item_tiles * (a.tile / kStep);
+    const int64_t cap = std::min<int64_t>(kMaxUnits, kMaxSteps / unit_steps);
+    if (const char *env = std::getenv("TRIATTN_UNITS_PER_WG")) {
+        const long forced = std::strtol(env, nullptr, 10);
+        if (forced >= 1)
+            return (int)std::max<int64_t>(1, std::min<int64_t>(forced, cap));
+    }
+    if (cap < 2 || unit_steps > kShortUnitSteps)
+        return 1;
+    const int64_t slots = std::max<int64_t>(1, 256 / a.hkv);
+    for (int64_t rounds = 1;; ++rounds) {
+        const int64_t upw = (units + slots * rounds - 1) / (slots * rounds);
+        if (upw <= cap)
+            return (int)upw;
+    }
+}
+
+ta_status launch_tiles(int kind, const FwdArgs &a_in, int32_t head_dim, int32_t max_item_tiles,
+                       hipStream_t stream)
+{
+    if (a_in.n_items <= 0)
         return TA_OK;
+    FwdArgs a = a_in;
     const int nw = a.group * a.rows_per_wg / 32;
-    dim3 grid((unsigned)((int64_t)a.n_items * a.subtiles * a.hkv));
-    hipError_t err = head_dim == 128 ? launch_tile<128>(nw, grid, a, kind, stream)
-                                     : launch_tile<64>(nw, grid, a, kind, stream);
+    const int64_t units = (int64_t)a.n_items * a.subtiles;
+    hipError_t err;
+    // Triangle passes over workgroups of five to eight waves run several
+    // units per workgroup (multi-unit kernel); the others one.
+    const int upw = units_per_wg(a, kind, nw, units, max_item_tiles);
+    if (upw > 1) {
+        a.n_units = (int32_t)units;
+        a.upw = upw;
+        a.n_slots = (int32_t)((units + upw - 1) / upw);
+        dim3 grid((unsigned)((int64_t)a.n_slots * a.hkv));
+        err = head_dim == 128 ? launch_units<128>(nw, grid, a, kind, stream)
+                              : launch_units<64>(nw, grid, a, kind, stream);
+    } else {
+        dim3 grid((unsigned)(units * a.hkv));
+        err = head_dim == 128 ? launch_tile<128>(nw, grid, a, kind, stream)
+                              : launch_tile<64>(nw, grid, a, kind, stream);
+    }
     if (err != hipSuccess)
         return fail(TA_ERR_HIP, "attention tile kernel launch failed: %s",
                     hipGetErrorString(err));
@@ -1269,7 +2121,8 @@ extern "C" ta_status triangle_attn_tiles(const void *q, const void *k, const voi
         return st;
     const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
                                 hq, hkv, softmax_scale, part_o, part_lse);
-    return launch_tiles(TA_KIND_TRIANGLE, a, head_dim, static_cast<hipStream_t>(stream));
+    return launch_tiles(TA_KIND_TRIANGLE, a, head_dim, info->max_item_tiles,
+                        static_cast<hipStream_t>(stream));
 }
 
 extern "C" ta_status triangle_attn_merge(void *o, int32_t o_dtype, float *lse,
@@ -1332,7 +2185,7 @@ ta_status split_pass_fwd(const char *fn, int kind, const void *q, const void *k,
     const hipStream_t s = static_cast<hipStream_t>(stream);
     const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
                                 hq, hkv, softmax_scale, part_o, part_lse);
-    st = launch_tiles(kind, a, head_dim, s);
+    st = launch_tiles(kind, a, head_dim, info->max_item_tiles, s);
     if (st != TA_OK)
         return st;
     return launch_merge(o, o_dtype, lse, sched_dev, info, total_tokens, hq, head_dim,
@@ -1455,5 +2308,6 @@ extern "C" ta_status causal_attn_fwd(const void *q, const void *k, const void *v
         return st;
     const FwdArgs a = make_args(q, k, v, o, o_dtype, lse, sched_dev, info, total_tokens,
                                 hq, hkv, softmax_scale, nullptr, nullptr);
-    return launch_tiles(TA_KIND_CAUSAL, a, head_dim, static_cast<hipStream_t>(stream));
+    return launch_tiles(TA_KIND_CAUSAL, a, head_dim, info->max_item_tiles,
+                        static_cast<hipStream_t>(stream));
 }

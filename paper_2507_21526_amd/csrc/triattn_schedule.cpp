@@ -138,6 +138,7 @@ extern "C" ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
     std::vector<Item> last_items, items;
     std::vector<Merge> merges;
     int64_t partial_rows = 0, kept = 0, last_rows_total = 0, max_splits = 0;
+    int64_t max_item = 0;
 
     for (int32_t b = 0; b < batch; ++b) {
         const int64_t off = cu_seqlens[b];
@@ -174,6 +175,7 @@ extern "C" ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
             }
             const int64_t cost = (ka1 - ka0) + (kb1 - kb0);
             kept += cost;
+            max_item = std::max(max_item, cost);
             Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
                         (int32_t)ka0, (int32_t)ka1, (int32_t)kb0, (int32_t)kb1,
                         kind == TA_KIND_CAUSAL ? kModeCausal : kModeStreaming,
@@ -190,6 +192,7 @@ extern "C" ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
             kept += nk;
             for (int64_t c = 0; c < ns; ++c) {
                 const int64_t k0 = c * nk / ns, k1 = (c + 1) * nk / ns;
+                max_item = std::max(max_item, k1 - k0);
                 Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
                             (int32_t)k0, (int32_t)k1, 0, 0, kModeCausal,
                             (int32_t)(partial_rows + c * (r1 - r0)),
@@ -239,6 +242,7 @@ extern "C" ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
     info->n_partial_rows = (int32_t)partial_rows;
     info->max_splits = (int32_t)max_splits;
     info->kept_tiles_per_qhead = kept;
+    info->max_item_tiles = (int32_t)max_item;
 
     if (!out)
         return TA_OK;
@@ -294,7 +298,7 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
                                               ceil_div(2 * listed, std::max<int64_t>(n_qtiles, 1)));
     std::vector<Item> split_items, items;
     std::vector<Merge> merges;
-    int64_t partial_rows = 0, merged_rows = 0, max_splits = 0;
+    int64_t partial_rows = 0, merged_rows = 0, max_splits = 0, max_item = 0;
     int64_t qt = 0;  // global q-tile index
 
     for (int32_t b = 0; b < batch; ++b) {
@@ -323,6 +327,7 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
             std::vector<Item> q_items;
             for (int64_t c = 0; c < ns; ++c) {
                 const int64_t a = c * len / ns, z = (c + 1) * len / ns;
+                max_item = std::max(max_item, z - a);
                 Item it = {{(int32_t)off, (int32_t)n, (int32_t)r0, (int32_t)r1,
                             (int32_t)(p0 + a), (int32_t)(z - a), 0, 0, kModeCausalList,
                             -1, (int32_t)(z - a), 0}};
@@ -373,6 +378,7 @@ extern "C" ta_status ta_build_blocksparse_schedule(const int32_t *cu_seqlens,
     info->n_partial_rows = (int32_t)partial_rows;
     info->max_splits = (int32_t)max_splits;
     info->kept_tiles_per_qhead = list_words;
+    info->max_item_tiles = (int32_t)max_item;
     if (!out)
         return TA_OK;
     if (out_words < words)
