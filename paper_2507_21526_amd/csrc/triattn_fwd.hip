@@ -257,7 +257,12 @@ __device__ __forceinline__ int vswz(int r)
     return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
 }
 
-template <int D, int NW>
+// COPIER: the last of the NW waves only copies K/V tiles into LDS (all of
+// them, at the start of each matrix phase of group 0) and computes nothing;
+// the other NW - 1 waves compute.  For GQA group 7 (seven waves of 32 rows),
+// whose eighth ping-pong slot would otherwise be empty: the MFMA waves then
+// issue no copies.
+template <int D, int NW, bool COPIER = false>
 __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(FwdArgs a,
                                                                                int32_t kind)
 {
@@ -269,8 +274,11 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     constexpr int ROWS_PER_DMA = 1024 / ROW_BYTES;      // rows per wave copy
     constexpr int N_DMA = kStep / ROWS_PER_DMA;         // wave copies per tile
     // Only the waves of ping-pong group 0 copy K/V tiles into LDS, spread
-    // over the MFMAs of their matrix phase (see the phase loop below).
-    constexpr int N_COPY_WAVES = NW - NW / 2;
+    // over the MFMAs of their matrix phase (see the phase loop below), or
+    // the copier wave alone.
+    static_assert(!COPIER || NW == 8, "a copier wave beside seven compute waves");
+    constexpr int NC = COPIER ? NW - 1 : NW;  // compute waves
+    constexpr int N_COPY_WAVES = COPIER ? 1 : NW - NW / 2;
     constexpr int COPIES = (N_DMA + N_COPY_WAVES - 1) / N_COPY_WAVES;  // per tile
     constexpr int QK_STEPS = D / 16;
     constexpr int D_BLOCKS = D / 32;
@@ -413,7 +421,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     const uint32_t smem_addr =
         (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)smem;
     const int q_row0 = min(row_base, r1 - 1);  // the wave's first row to read
-    {
+    if (!COPIER || wave < NC) {
         const uint16_t *qb = a.q + ((seq_off + q_row0) * a.hq + head) * (int64_t)D;
         const uint32_t q_pitch = (uint32_t)(a.hq * ROW_BYTES);
 #pragma unroll
@@ -442,7 +450,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // l / CHUNKS, stored chunk l % CHUNKS, which holds logical chunk
     // (l % CHUNKS) ^ swizzle(row).  Copy waves (group 0, wave w < N_COPY_WAVES)
     // own copies m = w, w + N_COPY_WAVES, ... of every K and V tile.
-    const bool copy_wave = wave < N_COPY_WAVES;
+    const bool copy_wave = COPIER ? wave == NW - 1 : wave < N_COPY_WAVES;
+    const int copy_rank = COPIER ? 0 : wave;  // the wave's first copy number
     const int dma_row_in = lane / CHUNKS;
     const int dma_pc = lane % CHUNKS;
     // The swizzle of row m * ROWS_PER_DMA + i is swizzle(i) ^ swizzle of the
@@ -454,7 +463,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // Byte offset of the row of the tile that this lane copies in the wave's
     // first copy, and the step from one of the wave's copies to the next.
     const uint32_t dma_off0 =
-        __umul24((uint32_t)(wave * ROWS_PER_DMA + dma_row_in), row_stride_bytes);
+        __umul24((uint32_t)(copy_rank * ROWS_PER_DMA + dma_row_in), row_stride_bytes);
     const uint32_t dma_off_step = (uint32_t)(N_COPY_WAVES * ROWS_PER_DMA) * row_stride_bytes;
     // The K swizzle term of copy i, kswz((wave + i * N_COPY_WAVES) *
     // ROWS_PER_DMA), does not depend on i when N_COPY_WAVES * ROWS_PER_DMA
@@ -486,12 +495,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         TileCopy t;
         t.base = src + (int64_t)kc * tok_stride;
         t.lim = (uint32_t)min(key_max - kc, kStep - 1) * row_stride_bytes;
-        t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0) + wave * 1024;
+        t.lds = smem_addr + buf * STAGE_BYTES + (is_v ? TILE_BYTES : 0) + copy_rank * 1024;
         return t;
     };
-    // Copy i of this wave (m = wave + i * N_COPY_WAVES) of a planned tile.
+    // Copy i of this wave (m = copy_rank + i * N_COPY_WAVES) of a planned tile.
     auto issue_copy = [&](const TileCopy &t, int i, bool is_v) TA_INLINE {
-        const int m = wave + i * N_COPY_WAVES;
+        const int m = copy_rank + i * N_COPY_WAVES;
         if constexpr (N_DMA % N_COPY_WAVES != 0) {
             if (m >= N_DMA)
                 return;
@@ -521,6 +530,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             issue_slot(slot / COPY_STRIDE);
     };
     auto no_hook = [](int) {};
+    // The hook of group 0's matrix phases: its copies, unless a copier wave
+    // makes them.
+    auto g0_hook = [&](int slot) TA_INLINE {
+        if constexpr (!COPIER)
+            copy_hook(slot);
+    };
 
     // S^T = K Q^T for one 64-key step from LDS stage `buf`; the two 32-key
     // accumulator chains alternate so that dependent MFMAs do not stall.
@@ -698,8 +713,10 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // 2j+1.  During M(j) the group-0 waves copy K(j+1) and V(j) into stage
     // (j+1) & 1 (last read in phase 2j-1), one copy after every COPY_STRIDE
     // MFMAs so that the address units see a steady stream, and wait for them
-    // at the end of phase 2j+1.  The softmax waves issue no copies.
-    const int n_group1 = NW / 2;
+    // at the end of phase 2j+1.  The softmax waves issue no copies.  With a
+    // copier wave (seven compute waves: four in group 0, three in group 1),
+    // that wave makes all of these copies and group 0 none.
+    const int n_group1 = NW / 2;  // the copier wave, if any, returns before
     const int group = NW >= 2 ? (wave >= NW - n_group1 ? 1 : 0) : 0;
     f32x16 s_acc[2];
     bf16x8 p_acc[2][2];
@@ -753,6 +770,33 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     using Stage0 = std::integral_constant<int, 0>;
     using Stage1 = std::integral_constant<int, 1>;
 
+    if constexpr (COPIER) {
+        // The copier wave: K(0) in the prologue, then for every step j the
+        // copies of K(j+1) and V(j) at the start of phase 2j, waited for at
+        // the end of phase 2j+1; its barriers match those of the other waves.
+        if (wave == NW - 1) {
+            if (nsteps > 0) {
+                cp_k = plan_copy(kbase, step_key0(0), 0, false);
+#pragma unroll
+                for (int c = 0; c < COPIES; ++c)
+                    issue_slot(c);
+                end_phase(true);
+                if constexpr (Q_IN_STAGE)
+                    end_phase(false);
+                for (int j = 0; j < nsteps; ++j) {
+                    plan_step_copies(j, j & 1);
+#pragma unroll
+                    for (int c = 0; c < 2 * COPIES; ++c)
+                        issue_slot(c);
+                    end_phase(false);
+                    end_phase(true);
+                }
+                end_phase(false);
+                end_phase(false);
+            }
+            return;
+        }
+    }
     if (nsteps > 0) {
         // Prologue: the copy waves copy K(0) into stage 0.
         if (copy_wave) {
@@ -767,19 +811,23 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             end_phase(false);  // stage 1 is free once every wave has read its Q
         if (group == 0) {
             // j = 0: QK only, then the copies of the PV slots.
-            plan_step_copies(0, Stage0{});
-            do_m(Stage0{}, true, false, copy_hook);
+            if constexpr (!COPIER)
+                plan_step_copies(0, Stage0{});
+            do_m(Stage0{}, true, false, g0_hook);
+            if constexpr (!COPIER) {
 #pragma unroll
-            for (int c = 0; c < 2 * COPIES; ++c)
-                if (c * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
-                    issue_slot(c);
+                for (int c = 0; c < 2 * COPIES; ++c)
+                    if (c * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
+                        issue_slot(c);
+            }
             end_phase(false);
             do_x(0);
             end_phase(true);
             // step j reads stage j & 1 (odd j first)
             auto step = [&](int j, auto stage) TA_INLINE {
-                plan_step_copies(j, stage);
-                do_m(stage, true, true, copy_hook);
+                if constexpr (!COPIER)
+                    plan_step_copies(j, stage);
+                do_m(stage, true, true, g0_hook);
                 end_phase(false);
                 do_x(j);
                 end_phase(true);
@@ -1849,7 +1897,8 @@ hipError_t launch_tile(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_
     case 4: hipLaunchKernelGGL((attn_tile_kernel<D, 4>), grid, dim3(256), 0, s, a, kind); break;
     case 5: hipLaunchKernelGGL((attn_tile_kernel<D, 5>), grid, dim3(320), 0, s, a, kind); break;
     case 6: hipLaunchKernelGGL((attn_tile_kernel<D, 6>), grid, dim3(384), 0, s, a, kind); break;
-    case 7: hipLaunchKernelGGL((attn_tile_kernel<D, 7>), grid, dim3(448), 0, s, a, kind); break;
+    // seven compute waves and a copier wave
+    case 7: hipLaunchKernelGGL((attn_tile_kernel<D, 8, true>), grid, dim3(512), 0, s, a, kind); break;
     case 8: hipLaunchKernelGGL((attn_tile_kernel<D, 8>), grid, dim3(512), 0, s, a, kind); break;
     default: return hipErrorInvalidValue;
     }
