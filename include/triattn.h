@@ -305,11 +305,15 @@ ta_status blocksparse_attn_fwd(const void *q, const void *k, const void *v,
  *                each sequence); all >= 0.  The paper probes with 64, 128,
  *                128 on ~2K-token prompts.
  *   workspace    device buffer of at least ta_probe_workspace_bytes(info,
- *                hq) bytes, 8-byte aligned (NULL when that is 0); its
- *                contents on entry do not matter.
+ *                hq) bytes (512 * tile / 32 * hq * 3 doubles; 0 for a
+ *                schedule without items), 8-byte aligned (NULL when that is
+ *                0); its contents on entry do not matter.
  * Grad(M-hat_r, l) = sum_h region_sums[h * 3 + r] / (hq * count_r) with the
- * pair counts of ta_region_counts (ta_region_grad_mean).  The result is
- * deterministic (fixed reduction order).  Errors as triangle_attn_fwd.
+ * pair counts of ta_region_counts (ta_region_grad_mean).  The work is cut
+ * into equal shares of kept k-tiles, one per workgroup, so the pass does not
+ * wait on the longest q-tile.  The result is deterministic (fixed shares and
+ * reduction order for a given shape).  Device schedule words that do not
+ * match info give NaN sums.  Errors as triangle_attn_fwd.
  */
 size_t ta_probe_workspace_bytes(const ta_schedule_info *info, int32_t hq);
 ta_status region_grad_probe(const void *q, const void *k, const void *v,

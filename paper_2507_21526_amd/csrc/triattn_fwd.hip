@@ -34,6 +34,7 @@
 #include <mutex>
 #include <type_traits>
 
+#include "triattn_device.h"
 #include "triattn_internal.h"
 
 // Library-owned device memory of triangle_attn_fwd_noalloc: the Last-row
@@ -46,18 +47,11 @@ static __device__ __align__(256) unsigned char scratch[TA_NOALLOC_SCRATCH_BYTES]
 namespace triattn {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-// Lambdas of the tile kernel are always inlined: the step loops call several
-// of them more than once and must not turn them into calls.
-#define TA_INLINE __attribute__((always_inline))
 
 constexpr int kStep = 64;  // keys per inner step
 constexpr int kKeyTable = 2048;  // LDS table of a list item's step keys
@@ -176,66 +170,6 @@ __device__ __forceinline__ float pair_sum(float x)
 // when a step's probabilities against the stale maximum could exceed this
 // bound (2^8), so every probability stays at most 2^8.
 constexpr float kRescaleBound = 256.0f;
-
-// Register fences: an empty volatile asm that reads and rewrites a value, so
-// the computation producing it cannot be moved past this point (side-effect
-// free arithmetic could otherwise be sunk across a phase boundary).
-__device__ __forceinline__ void fence_regs(bf16x8 &x)
-{
-    asm volatile("" : "+v"(x));
-}
-__device__ __forceinline__ void fence_regs(float &x)
-{
-    asm volatile("" : "+v"(x));
-}
-
-// One wave-wide 16-byte-per-lane copy from global memory straight into LDS
-// (lane l lands at lds_addr + 16 l).  Issued from inline assembly so that the
-// compiler does not serialise it against unrelated LDS reads (the copy
-// targets the other LDS stage; barriers order it against the readers of its
-// own stage): completion is tracked explicitly with vmcnt waits.  The LDS
-// address is bound to M0 through the operand constraint, so the compiler
-// writes M0 itself (one scalar add per copy) and knows its value; the nop
-// is the wait state between that write and the copy reading it.
-__device__ __forceinline__ void copy_to_lds16(const void *gbase, uint32_t lane_byte_off,
-                                              uint32_t lds_addr)
-{
-    asm volatile("s_nop 0\n\t"
-                 "global_load_lds_dwordx4 %0, %1"
-                 :
-                 : "v"(lane_byte_off), "s"(gbase), "{m0}"(lds_addr));
-}
-
-// Workgroup barrier without a memory fence: this wave's LDS reads are
-// complete (lgkmcnt 0); copies into LDS are synchronised by vmcnt waits.
-__device__ __forceinline__ void barrier_no_fence()
-{
-    asm volatile("" ::: "memory");       // no compiler motion of memory ops
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
-
-// s_waitcnt vmcnt(n) for a run-time n (small): the count is an immediate.
-__device__ __forceinline__ void wait_vmcnt(int n)
-{
-    // expcnt and lgkmcnt fields left at their maximum (no wait on them)
-    switch (n) {
-    case 0: __builtin_amdgcn_s_waitcnt(0x0f70); break;
-    case 1: __builtin_amdgcn_s_waitcnt(0x0f71); break;
-    case 2: __builtin_amdgcn_s_waitcnt(0x0f72); break;
-    case 3: __builtin_amdgcn_s_waitcnt(0x0f73); break;
-    case 4: __builtin_amdgcn_s_waitcnt(0x0f74); break;
-    case 5: __builtin_amdgcn_s_waitcnt(0x0f75); break;
-    case 6: __builtin_amdgcn_s_waitcnt(0x0f76); break;
-    case 7: __builtin_amdgcn_s_waitcnt(0x0f77); break;
-    default: __builtin_amdgcn_s_waitcnt(0x0f78); break;
-    }
-}
-
-// Instruction classes of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSchedMfma = 0x008;
-constexpr int kSchedDsRead = 0x100;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;

@@ -10,17 +10,24 @@
 // last), which partition the causal mask; Sec. 3 ranks layers by the middle
 // section's value to choose the Triangle layers.
 //
-// Probe kernel: a workgroup owns one work item of a causal schedule (a q-tile
-// and its k-tiles up to the diagonal), one kv head g and R rows of each of
-// the G query heads of g, so every K/V tile staged in LDS serves the whole
-// GQA group.  Each wave owns 32 rows of one head.  Per 64-key step it runs
+// Probe kernel: a workgroup owns one kv head g, one block of R rows of each
+// q-tile for each of the G query heads of g (so every K/V tile staged in
+// LDS serves the whole GQA group) and one slot: an equal share of the kept
+// k-tiles of the causal schedule's work items (a q-tile and its k-tiles up
+// to the diagonal), the items laid end to end in schedule order.  A share
+// is a run of chunks (an item's k-tiles from s0 to s1), so a q-tile's
+// k-tiles may be spread over two or more workgroups: the probe's sums are
+// additive over key ranges, and equal shares keep the pass from waiting on
+// the longest q-tile (at 2K tokens one item per workgroup leaves the
+// diagonal's last q-tile with 16 k-tiles against a mean of 8.5).  Each wave
+// owns 32 rows of one head.  Per 64-key step it runs
 // two bf16 MFMA 32x32x16 contractions with the same operand layout, S^T =
 // K Q^T and dP^T = V dO^T (keys on the MFMA rows, queries on the columns), so
 // a lane holds matching entries of both: it forms A = 2^(S c - lse log2 e)
 // (c = scale log2 e; the row's LSE is an input, so no softmax state is
 // carried) and adds A dP to the accumulator of the pair's section.  Per-step
 // fp32 sums go into fp64 lane accumulators; each wave reduces them and writes
-// one fp64 partial per (32-row block, head, section).  The reduce kernel sums
+// one fp64 partial per (slot, 32-row block, head, section).  The reduce kernel sums
 // the partials of each (head, section) in a fixed order, so results are
 // deterministic.  Roofline: MFMA, 4 T^2 d flops per kept (q-tile, k-tile)
 // pair and head, as the forward pass.
@@ -29,20 +36,21 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <numeric>
+#include <type_traits>
 #include <vector>
 
+#include "triattn_device.h"
 #include "triattn_internal.h"
 
 namespace triattn {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
 constexpr int kProbeStep = 64;  // keys per step
 constexpr float kProbeLog2e = 1.4426950408889634f;
+constexpr int kProbeCUs = 256;       // compute units of the MI355X
+constexpr int kProbeMaxSlots = 512;  // workgroups per (kv head, row block), at most
 
 struct ProbeArgs {
     const uint16_t *q;
@@ -51,7 +59,7 @@ struct ProbeArgs {
     const uint16_t *dout;
     const float *lse;     // [hq, total] natural log
     const int32_t *sched;
-    double *part;         // [n_items * tile / 32, hq, 3]
+    double *part;         // [n_slots * tile / 32, hq, 3]
     int64_t total_tokens;
     int32_t hq, hkv, group;
     int32_t n_items;
@@ -60,6 +68,9 @@ struct ProbeArgs {
     int32_t subtiles;     // tile / R
     int32_t sink, window, last;
     float scale_log2;     // softmax scale * log2(e)
+    int32_t n_slots;      // workgroups per (kv head, row block)
+    int32_t per_item;     // 1: workgroup slot runs item slot whole
+    int64_t total_cost;   // kept k-tiles per head (the items' costs summed)
 };
 
 // 16-byte chunk swizzle of LDS row r: the 32 rows one operand fetch reads
@@ -71,29 +82,37 @@ __device__ __forceinline__ int probe_swz(int r)
 }
 
 __device__ __forceinline__ bool probe_header_ok(const int32_t *s, int64_t total,
-                                                int32_t n_items, int32_t tile)
+                                                int32_t n_items, int32_t tile, int64_t kept)
 {
     const int64_t t = (int64_t)(uint32_t)s[H_TOTAL_LO] | ((int64_t)s[H_TOTAL_HI] << 32);
     return s[H_MAGIC] == TA_SCHEDULE_MAGIC && s[H_VERSION] == TA_SCHEDULE_VERSION &&
            s[H_KIND] == TA_KIND_CAUSAL && s[H_TILE] == tile && t == total &&
-           s[H_ITEMS] == n_items;
+           s[H_ITEMS] == n_items && s[H_KEPT_TILES] == kept;
 }
 
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void probe_kernel(ProbeArgs a)
+__global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeArgs a)
 {
-    constexpr int CH = D / 8;                        // 16-byte chunks per row
-    constexpr int TILE_BYTES = kProbeStep * D * 2;   // one bf16 K or V tile
-    constexpr int STAGE_BYTES = 2 * TILE_BYTES;      // K then V
-    constexpr int CHUNKS = 2 * kProbeStep * CH;      // chunks per stage
+    constexpr int ROW_BYTES = 2 * D;
+    constexpr int CHUNKS = D / 8;                       // 16-byte chunks per row
+    constexpr int TILE_BYTES = kProbeStep * ROW_BYTES;  // one K or V tile
+    constexpr int STAGE_BYTES = 2 * TILE_BYTES;         // K tile, then V tile
+    constexpr int ROWS_PER_DMA = 1024 / ROW_BYTES;      // rows per wave copy
+    constexpr int N_DMA = kProbeStep / ROWS_PER_DMA;    // wave copies per tile
+    constexpr int N_COPY_WAVES = NW - NW / 2;           // the waves of group 0
+    constexpr int COPIES = (N_DMA + N_COPY_WAVES - 1) / N_COPY_WAVES;  // per tile
+    constexpr int QK = D / 16;                          // MFMA k-steps over d
+    constexpr int MFMA_SLOTS = 4 * QK;                  // MFMAs of a matrix phase
+    constexpr int COPY_STRIDE = MFMA_SLOTS / (2 * COPIES) > 0
+                                    ? MFMA_SLOTS / (2 * COPIES) : 1;
     constexpr int NT = NW * 64;
-    constexpr int CPT = (CHUNKS + NT - 1) / NT;      // chunks per thread
-    constexpr int QK = D / 16;                       // MFMA k-steps over d
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE_BYTES];
+    __shared__ int64_t wave_tot[NW];
+    __shared__ int64_t first[2];  // first item of the share, its cost prefix
 
-    const int per_item = a.subtiles * a.hkv;
-    const int item = blockIdx.x / per_item;
-    const int rem = blockIdx.x - item * per_item;
+    const int per_slot = a.subtiles * a.hkv;
+    const int slot = blockIdx.x / per_slot;
+    const int rem = blockIdx.x - slot * per_slot;
     const int g = rem / a.subtiles;
     const int sub = rem - g * a.subtiles;
 
@@ -104,37 +123,162 @@ __global__ __launch_bounds__(NW * 64) void probe_kernel(ProbeArgs a)
     const int wph = a.rows_per_wg / 32;  // waves per head
     const int head = g * a.group + wave / wph;
     const int rb = sub * wph + wave % wph;  // 32-row block within the q-tile
-
-    double acc_s = 0.0, acc_o = 0.0;  // streaming / other (middle or last)
-    bool last_row = false;
+    // Ping-pong groups as in the forward tile kernel: waves w and w + 4
+    // share a SIMD and sit in different groups; group 0 copies the K/V tiles.
+    const int group = wave >= NW - NW / 2 ? 1 : 0;
+    const bool copy_wave = wave < N_COPY_WAVES;
 
     const int32_t *sched = a.sched;
-    bool ok = probe_header_ok(sched, a.total_tokens, a.n_items, a.tile);
-    int64_t seq_off = 0;
-    int32_t seq_len = 0, r0 = 0, r1 = 0, ka0 = 0, ka1 = 0;
-    if (ok) {
+    bool ok = probe_header_ok(sched, a.total_tokens, a.n_items, a.tile, a.total_cost);
+    // The workgroup's share of kept k-tiles [lo, hi), counted over the items
+    // laid end to end in schedule order from `pre` at item `item`: one whole
+    // item (per-item launch), or an equal share of the total.
+    int item = 0;
+    int64_t pre = 0, lo = 0, hi = 0;
+    if (ok && a.per_item) {
+        item = slot;
+        hi = sched[kHdrWords + (int64_t)item * kItemWords + I_COST];
+    } else if (ok) {
+        const int64_t per = (a.total_cost + a.n_slots - 1) / a.n_slots;
+        lo = min((int64_t)slot * per, a.total_cost);
+        hi = min(lo + per, a.total_cost);
+        if (lo < hi) {
+            // Item holding k-tile lo: thread t sums the costs of items
+            // [t m, t m + m), a scan over the threads gives each its prefix,
+            // and the thread whose items contain lo records it.  The costs
+            // must add up to the header's total, none negative.
+            const int m = (a.n_items + NT - 1) / NT;
+            const int i0 = min(tid * m, a.n_items), i1 = min(i0 + m, a.n_items);
+            auto cost_of = [&](int i) -> int64_t {
+                return sched[kHdrWords + (int64_t)i * kItemWords + I_COST];
+            };
+            int64_t tsum = 0;
+            bool neg = false;
+            for (int i = i0; i < i1; ++i) {
+                const int64_t c = cost_of(i);
+                neg |= c < 0;
+                tsum += c;
+            }
+            int64_t x = tsum;  // inclusive scan over the wave
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int64_t y = __shfl_up(x, o);
+                if (lane >= o)
+                    x += y;
+            }
+            if (lane == 63)
+                wave_tot[wave] = x;
+            if (tid == 0)
+                first[0] = -1;
+            __syncthreads();
+            int64_t p = x - tsum, total = 0;
+            for (int w = 0; w < NW; ++w) {
+                p += w < wave ? wave_tot[w] : 0;
+                total += wave_tot[w];
+            }
+            for (int i = i0; i < i1; ++i) {
+                const int64_t c = cost_of(i);
+                if (p <= lo && lo < p + c) {
+                    first[0] = i;
+                    first[1] = p;
+                }
+                p += c;
+            }
+            ok = !__syncthreads_or(neg) && total == a.total_cost && first[0] >= 0;
+            item = __builtin_amdgcn_readfirstlane((int)first[0]);
+            pre = first[1];
+        }
+    }
+
+    const float c = a.scale_log2;
+    const int tok_stride = a.hkv * D;
+    const uint32_t row_stride_bytes = 2u * (uint32_t)tok_stride;  // < 2^24 (host check)
+    const uint32_t smem_addr =
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)lds;
+
+    // A operand offsets: lane row r = lane % 32 of a 32-row half, chunk
+    // (2 s + h) ^ swizzle(r); the second half (rows 32-63) adds 32 rows (its
+    // swizzle is the same).
+    const int r_lane = lane & 31;
+    uint32_t aoff[QK];
+#pragma unroll
+    for (int s = 0; s < QK; ++s)
+        aoff[s] = (uint32_t)(r_lane * ROW_BYTES + (((2 * s + h) ^ probe_swz<D>(r_lane)) << 4));
+
+    // Copy m of a tile writes its rows m * ROWS_PER_DMA .. (1 KB): lane l
+    // lands at row m * ROWS_PER_DMA + l / CHUNKS, stored chunk l % CHUNKS,
+    // which holds logical chunk (l % CHUNKS) ^ swizzle(row); rows past the
+    // last key of the sequence read that key (masked).  Group-0 wave w makes
+    // copies m = w, w + N_COPY_WAVES, ... of each K and V tile.
+    const int dma_row_in = lane / CHUNKS;
+    const int dma_pc = lane % CHUNKS;
+    struct TileCopy {
+        const uint16_t *kb, *vb;  // row kc of K and V
+        uint32_t lim;             // min(last key - kc, 63) * row pitch in bytes
+        uint32_t lds;             // LDS address of the stage
+    };
+    TileCopy cp{};
+    auto issue_copy = [&](int i, bool is_v) TA_INLINE {
+        const int m = wave + i * N_COPY_WAVES;
+        if constexpr (N_DMA % N_COPY_WAVES != 0) {
+            if (m >= N_DMA)
+                return;
+        }
+        const int row = m * ROWS_PER_DMA + dma_row_in;
+        const uint32_t off = min(__umul24((uint32_t)row, row_stride_bytes), cp.lim) +
+                             (uint32_t)((dma_pc ^ probe_swz<D>(row)) << 4);
+        copy_to_lds16(is_v ? cp.vb : cp.kb, off,
+                      cp.lds + (is_v ? TILE_BYTES : 0) + m * 1024);
+    };
+    auto issue_slot = [&](int cc) TA_INLINE {
+        if (cc < COPIES)
+            issue_copy(cc, false);
+        else
+            issue_copy(cc - COPIES, true);
+    };
+    auto copy_hook = [&](int slot_) TA_INLINE {
+        if (slot_ % COPY_STRIDE == COPY_STRIDE - 1 && slot_ / COPY_STRIDE < 2 * COPIES)
+            issue_slot(slot_ / COPY_STRIDE);
+    };
+    auto no_hook = [](int) {};
+    auto end_phase = [&](bool wait_copies) TA_INLINE {
+        __builtin_amdgcn_sched_barrier(0);
+        if (wait_copies)
+            wait_vmcnt(0);
+        barrier_no_fence();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    using Stage0 = std::integral_constant<int, 0>;
+    using Stage1 = std::integral_constant<int, 1>;
+
+    double acc_s = 0.0, acc_m = 0.0, acc_l = 0.0;  // streaming / middle / last
+    for (; ok && item < a.n_items && pre < hi; ++item) {
         const int32_t *it = sched + kHdrWords + (int64_t)item * kItemWords;
-        seq_off = it[I_SEQ_OFF];
-        seq_len = it[I_SEQ_LEN];
-        r0 = it[I_R0];
-        r1 = it[I_R1];
-        ka0 = it[I_KA0];
-        ka1 = it[I_KA1];
+        const int64_t seq_off = it[I_SEQ_OFF];
+        const int32_t seq_len = it[I_SEQ_LEN];
+        const int32_t r0 = it[I_R0], r1 = it[I_R1];
+        const int32_t ka0 = it[I_KA0], ka1 = it[I_KA1];
+        const int64_t cost = it[I_COST];
         // guard against a malformed schedule: never touch memory outside it
         ok = it[I_MODE] == kModeCausal && it[I_KB0] == it[I_KB1] && seq_off >= 0 &&
              seq_len > 0 && seq_off + seq_len <= a.total_tokens && r0 >= 0 && r0 < r1 &&
-             r1 <= seq_len && ka0 >= 0 && ka1 >= ka0;
-    }
-    const int wr0 = r0 + sub * a.rows_per_wg;  // first row of this workgroup
-    ok = ok && wr0 < r1;                       // uniform over the workgroup
+             r1 <= seq_len && ka0 >= 0 && ka1 >= ka0 && cost == ka1 - ka0 &&
+             ka1 <= (seq_len + a.tile - 1) / a.tile;
+        if (!ok)
+            break;
+        const int s0 = (int)max<int64_t>(lo - pre, 0);
+        const int s1 = (int)min<int64_t>(hi - pre, cost);
+        pre += cost;
+        const int wr0 = r0 + sub * a.rows_per_wg;  // first row of this workgroup
+        if (wr0 >= r1)
+            continue;  // ragged q-tile: no rows here (uniform)
 
-    if (ok) {
         const int row_base = wr0 + (wave % wph) * 32;
-        const int my_row = row_base + (lane & 31);
+        const int my_row = row_base + r_lane;
         const bool row_valid = my_row < r1;
         const int load_row = row_valid ? my_row : r1 - 1;
-        last_row = my_row >= seq_len - min(a.last, seq_len);
-        const float c = a.scale_log2;
+        const int row_hi = min(row_base + 31, r1 - 1);  // last valid row of the wave
+        const bool last_row = my_row >= seq_len - min(a.last, seq_len);
         const float lse2 = a.lse[(int64_t)head * a.total_tokens + seq_off + load_row] *
                            kProbeLog2e;
 
@@ -151,117 +295,192 @@ __global__ __launch_bounds__(NW * 64) void probe_kernel(ProbeArgs a)
 
         // keys past the workgroup's last row are masked for all its rows
         const int wg_last = min(wr0 + a.rows_per_wg, r1) - 1;
-        const int key_begin = ka0 * a.tile;
-        const int key_end = min(ka1 * a.tile, wg_last + 1);
-        const int nsteps = key_end > key_begin ? (key_end - key_begin + kProbeStep - 1) / kProbeStep : 0;
-
-        // K/V staging: chunk x of a stage is tensor x / (64 CH) (0 = K, 1 =
-        // V), row (x / CH) % 64, chunk column x % CH; rows past the
-        // sequence repeat its last key (those keys are masked).
-        u32x4 pf[CPT];
-        auto load_step = [&](int s) {
-            const int key0 = key_begin + s * kProbeStep;
-#pragma unroll
-            for (int i = 0; i < CPT; ++i) {
-                const int x = tid + i * NT;
-                if (CHUNKS % NT == 0 || x < CHUNKS) {
-                    const int tensor = x / (kProbeStep * CH);
-                    const int row = (x / CH) % kProbeStep;
-                    const int col = x % CH;
-                    const int key = min(key0 + row, seq_len - 1);
-                    const uint16_t *src = (tensor ? a.v : a.k) +
-                                          ((seq_off + key) * a.hkv + g) * (int64_t)D + col * 8;
-                    pf[i] = *reinterpret_cast<const u32x4 *>(src);
-                }
-            }
-        };
-        auto store_step = [&](int stage) {
-#pragma unroll
-            for (int i = 0; i < CPT; ++i) {
-                const int x = tid + i * NT;
-                if (CHUNKS % NT == 0 || x < CHUNKS) {
-                    const int tensor = x / (kProbeStep * CH);
-                    const int row = (x / CH) % kProbeStep;
-                    const int col = x % CH;
-                    uint8_t *dst = lds + stage * STAGE_BYTES + tensor * TILE_BYTES +
-                                   row * (D * 2) + ((col ^ probe_swz<D>(row)) << 4);
-                    *reinterpret_cast<u32x4 *>(dst) = pf[i];
-                }
-            }
+        const int key_begin = (ka0 + s0) * a.tile;
+        const int key_end = min((ka0 + s1) * a.tile, wg_last + 1);
+        const int nsteps =
+            key_end > key_begin ? (key_end - key_begin + kProbeStep - 1) / kProbeStep : 0;
+        const int key_max = seq_len - 1;
+        const uint16_t *kbase = a.k + (seq_off * a.hkv + g) * (int64_t)D;
+        const uint16_t *vbase = a.v + (seq_off * a.hkv + g) * (int64_t)D;
+        // K and V tiles of step j into LDS stage `buf`
+        auto plan_copies = [&](int j, int buf) TA_INLINE {
+            const int kc = min(key_begin + j * kProbeStep, key_max);
+            cp.kb = kbase + (int64_t)kc * tok_stride;
+            cp.vb = vbase + (int64_t)kc * tok_stride;
+            cp.lim = (uint32_t)min(key_max - kc, kProbeStep - 1) * row_stride_bytes;
+            cp.lds = smem_addr + buf * STAGE_BYTES;
         };
 
-        auto compute = [&](const uint8_t *st, int key0) {
-            f32x16 sacc[2], gacc[2];
+        f32x16 sacc[2], gacc[2];
+        // Matrix phase of step j from LDS stage `stage`: S^T = K Q^T and
+        // dP^T = V dO^T for the two 32-key halves, the four accumulator
+        // chains interleaved so that dependent MFMAs do not stall.
+        auto do_m = [&](auto stage, auto hook) TA_INLINE {
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(1);  // MFMA issue goes first on the SIMD
+            __builtin_amdgcn_sched_barrier(0);
+            const uint8_t *kt = lds + (int)stage * STAGE_BYTES;
+            const uint8_t *vt = kt + TILE_BYTES;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
-                const int r = kb * 32 + (lane & 31);
-                const uint8_t *krow = st + r * (D * 2);
-                const uint8_t *vrow = st + TILE_BYTES + r * (D * 2);
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    sacc[kb][e] = 0.f;
-                    gacc[kb][e] = 0.f;
-                }
-#pragma unroll
-                for (int s = 0; s < QK; ++s) {
-                    const int off = ((2 * s + h) ^ probe_swz<D>(r)) << 4;
-                    const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(krow + off);
-                    const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(vrow + off);
-                    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
-                    gacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, df[s], gacc[kb], 0, 0, 0);
-                }
+                sacc[kb] = f32x16{};
+                gacc[kb] = f32x16{};
             }
-            // register e of lane half h holds key key0 + 32 kb + (e & 3) +
-            // 4 h + 8 (e >> 2) of this lane's row
-            const bool all_causal = key0 + kProbeStep - 1 <= row_base && row_base + 31 < r1;
-            const bool no_stream = key0 >= a.sink && row_base - (key0 + kProbeStep - 1) >= a.window;
-            float ss = 0.f, so = 0.f;
-            if (all_causal && no_stream) {
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+            for (int s = 0; s < QK; ++s) {
+                const bf16x8 k0 = *reinterpret_cast<const bf16x8 *>(kt + aoff[s]);
+                const bf16x8 v0 = *reinterpret_cast<const bf16x8 *>(vt + aoff[s]);
+                const bf16x8 k1 =
+                    *reinterpret_cast<const bf16x8 *>(kt + aoff[s] + 32 * ROW_BYTES);
+                const bf16x8 v1 =
+                    *reinterpret_cast<const bf16x8 *>(vt + aoff[s] + 32 * ROW_BYTES);
+                sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[s], sacc[0], 0, 0, 0);
+                hook(4 * s);
+                gacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v0, df[s], gacc[0], 0, 0, 0);
+                hook(4 * s + 1);
+                sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[s], sacc[1], 0, 0, 0);
+                hook(4 * s + 2);
+                gacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v1, df[s], gacc[1], 0, 0, 0);
+                hook(4 * s + 3);
+            }
+            // keep six operand reads in flight ahead of the MFMAs
+            constexpr int n = MFMA_SLOTS, ahead = 6;
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
 #pragma unroll
-                    for (int e = 0; e < 16; ++e)
-                        so += __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], c, -lse2)) * gacc[kb][e];
+            for (int i = 0; i < n - ahead; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(0);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+
+        // Vector phase of step j: A dP per pair, summed per section.  Register
+        // e of half kb holds key key0 + o(kb, e) + 4 h, o = 32 kb + (e & 3) +
+        // 8 (e >> 2).  A step whose pairs are all of one section (streaming or
+        // not) needs at most the causal test; only steps across a section
+        // edge classify each pair.  Rows past the q-tile are dropped when the
+        // chunk ends.
+        double chunk_s = 0.0, chunk_o = 0.0;  // streaming / other (middle or last)
+        auto do_x = [&](int j) TA_INLINE {
+            const int key0 = key_begin + j * kProbeStep;
+            const int lim = my_row - key0 - 4 * h;  // causal: o <= lim
+            const bool causal_all = key0 + kProbeStep - 1 <= row_base;
+            const bool strm_all = key0 + kProbeStep - 1 < a.sink || row_hi - key0 < a.window;
+            const bool strm_none =
+                key0 >= a.sink && row_base - (key0 + kProbeStep - 1) >= a.window;
+            float ts = 0.f, to = 0.f;
+            if (strm_all || strm_none) {
+                float t = 0.f;
+                if (causal_all) {
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            t += __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], c, -lse2)) *
+                                 gacc[kb][e];
+                } else {
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e) {
+                            const int o = 32 * kb + (e & 3) + 8 * (e >> 2);
+                            const float pr =
+                                __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], c, -lse2)) *
+                                gacc[kb][e];
+                            t += o <= lim ? pr : 0.f;
+                        }
+                }
+                ts = strm_all ? t : 0.f;
+                to = strm_all ? 0.f : t;
             } else {
+                const int slim = a.sink - key0 - 4 * h;  // sink key: o < slim
+                const int wlim = lim - a.window;          // in the window: o > wlim
+                float tv = 0.f;
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                     for (int e = 0; e < 16; ++e) {
-                        const int key = key0 + 32 * kb + (e & 3) + 4 * h + 8 * (e >> 2);
-                        const float p =
+                        const int o = 32 * kb + (e & 3) + 8 * (e >> 2);
+                        const float pr =
                             __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], c, -lse2)) * gacc[kb][e];
-                        const bool valid = row_valid && key <= my_row;
-                        const bool strm = key < a.sink || my_row - key < a.window;
-                        ss += (valid && strm) ? p : 0.f;
-                        so += (valid && !strm) ? p : 0.f;
+                        const float pv = o <= lim ? pr : 0.f;
+                        tv += pv;
+                        ts += ((o < slim) | (o > wlim)) ? pv : 0.f;
                     }
+                to = tv - ts;
             }
-            acc_s += (double)ss;
-            acc_o += (double)so;
+            chunk_s += (double)ts;
+            chunk_o += (double)to;
+            fence_regs(chunk_s);
+            fence_regs(chunk_o);
         };
 
+        // Two-group ping-pong over the steps (the forward tile kernel's
+        // schedule, with both operands of a step in one stage): group 0 runs
+        // the matrix phase of step j in phase 2j and its vector phase in
+        // phase 2j+1, group 1 one phase later.  Stage j & 1 holds K(j) and
+        // V(j); during its matrix phase of step j group 0 copies K(j+1) and
+        // V(j+1) into stage (j+1) & 1 (last read in phase 2j-1) and waits for
+        // them at the end of phase 2j+1.  The last step's copies repeat its
+        // own tiles into the other stage, which nobody reads.
         if (nsteps > 0) {
-            load_step(0);
-            store_step(0);
-            if (nsteps > 1)
-                load_step(1);
-            __syncthreads();
-            for (int s = 0; s < nsteps; ++s) {
-                compute(lds + (s & 1) * STAGE_BYTES, key_begin + s * kProbeStep);
-                if (s + 1 < nsteps) {
-                    // stage (s + 1) & 1 was last read in step s - 1, before
-                    // the barrier that ended it
-                    store_step((s + 1) & 1);
-                    if (s + 2 < nsteps)
-                        load_step(s + 2);
+            if (copy_wave) {
+                plan_copies(0, 0);
+#pragma unroll
+                for (int cc = 0; cc < 2 * COPIES; ++cc)
+                    issue_slot(cc);
+            }
+            end_phase(true);  // K(0) and V(0) have landed
+            if (group == 0) {
+                auto step = [&](int j, auto stage) TA_INLINE {
+                    plan_copies(min(j + 1, nsteps - 1), 1 - (int)stage);
+                    do_m(stage, copy_hook);
+                    end_phase(false);
+                    do_x(j);
+                    end_phase(true);
+                };
+                int j = 0;
+                for (; j + 1 < nsteps; j += 2) {
+                    step(j, Stage0{});
+                    step(j + 1, Stage1{});
                 }
-                __syncthreads();
+                if (j < nsteps)
+                    step(j, Stage0{});
+                end_phase(false);  // group 1's last vector phase
+            } else {
+                end_phase(false);  // group 0's first matrix phase
+                do_m(Stage0{}, no_hook);
+                end_phase(false);
+                auto step = [&](int j, auto stage) TA_INLINE {
+                    do_x(j - 1);
+                    end_phase(false);
+                    do_m(stage, no_hook);
+                    end_phase(false);
+                };
+                int j = 1;
+                for (; j + 1 < nsteps; j += 2) {
+                    step(j, Stage1{});
+                    step(j + 1, Stage0{});
+                }
+                if (j < nsteps)
+                    step(j, Stage1{});
+                do_x(nsteps - 1);
+                end_phase(false);
             }
         }
+        if (row_valid) {
+            acc_s += chunk_s;
+            if (last_row)
+                acc_l += chunk_o;
+            else
+                acc_m += chunk_o;
+        }
     }
+    ok = ok && pre >= hi;  // the items cover the share
 
-    double acc_m = last_row ? 0.0 : acc_o;
-    double acc_l = last_row ? acc_o : 0.0;
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
         acc_s += __shfl_xor(acc_s, off);
@@ -269,12 +488,14 @@ __global__ __launch_bounds__(NW * 64) void probe_kernel(ProbeArgs a)
         acc_l += __shfl_xor(acc_l, off);
     }
     if (lane == 0) {
-        // every partial is written (zero for rows past the q-tile), so the
-        // workspace needs no clearing
-        double *p = a.part + (((int64_t)item * (a.tile / 32) + rb) * a.hq + head) * 3;
-        p[0] = acc_s;
-        p[1] = acc_m;
-        p[2] = acc_l;
+        // every partial is written (zero for an empty share), so the
+        // workspace needs no clearing; a schedule that does not match the
+        // call gives NaN sums
+        double *pp = a.part + (((int64_t)slot * (a.tile / 32) + rb) * a.hq + head) * 3;
+        const double bad = __builtin_nan("");
+        pp[0] = ok ? acc_s : bad;
+        pp[1] = ok ? acc_m : bad;
+        pp[2] = ok ? acc_l : bad;
     }
 }
 
@@ -301,10 +522,46 @@ __global__ __launch_bounds__(256) void probe_reduce_kernel(const double *part, i
 
 int probe_rows_per_wg(int group, int tile)
 {
+    int max_waves = 8;
+    if (const char *env = std::getenv("TRIATTN_PROBE_WAVES")) {
+        const long forced = std::strtol(env, nullptr, 10);
+        if (forced >= 1 && forced <= 8)
+            max_waves = (int)forced;
+    }
     for (int r = 128; r >= 32; r /= 2)
-        if (r <= tile && group * r / 32 <= 8)
+        if (r <= tile && group * r / 32 <= max_waves)
             return r;
     return 32;
+}
+
+// Work split of the probe over the workgroups of one (kv head, row block).
+// Equal shares of the kept k-tiles, one workgroup each, as many as fill
+// every compute unit's resident workgroups once (two for workgroups of at
+// most four waves, whose registers and LDS leave room for two per CU, else
+// one), when the schedule's longest item is more than half a share: then one
+// item per workgroup would leave the pass waiting on the longest q-tile (at
+// 2K tokens: 16 k-tiles against a mean of 8.5).  Otherwise one workgroup per
+// item, in schedule order (heaviest first): the workgroups running at a time
+// then walk the same keys in step and share them in L2.  The environment
+// variable TRIATTN_PROBE_SLOTS, read at every call, forces equal shares of
+// that count (1 .. kProbeMaxSlots): for tests.
+struct ProbeSplit {
+    int64_t slots;
+    bool per_item;
+};
+ProbeSplit probe_split(int nw, int64_t wgs_per_slot, const ta_schedule_info *info)
+{
+    if (const char *env = std::getenv("TRIATTN_PROBE_SLOTS")) {
+        const long forced = std::strtol(env, nullptr, 10);
+        if (forced >= 1)
+            return {std::min<int64_t>(forced, kProbeMaxSlots), false};
+    }
+    const int64_t resident = (int64_t)kProbeCUs * (nw <= 4 ? 2 : 1);
+    const int64_t slots =
+        std::max<int64_t>(1, std::min<int64_t>(kProbeMaxSlots, resident / wgs_per_slot));
+    if ((int64_t)info->max_item_tiles * slots * 2 <= info->kept_tiles_per_qhead)
+        return {info->n_items, true};
+    return {slots, false};
 }
 
 template <int D>
@@ -331,7 +588,9 @@ extern "C" size_t ta_probe_workspace_bytes(const ta_schedule_info *info, int32_t
 {
     if (!info || hq <= 0 || info->n_items <= 0 || info->tile < 32)
         return 0;
-    return (size_t)info->n_items * (size_t)(info->tile / 32) * (size_t)hq * 3 * sizeof(double);
+    // one partial per (workgroup slot, 32-row block, head, section)
+    const size_t slots = (size_t)std::max<int64_t>(info->n_items, kProbeMaxSlots);
+    return slots * (size_t)(info->tile / 32) * (size_t)hq * 3 * sizeof(double);
 }
 
 extern "C" ta_status region_grad_probe(const void *q, const void *k, const void *v,
@@ -396,8 +655,14 @@ extern "C" ta_status region_grad_probe(const void *q, const void *k, const void 
     const int group = hq / hkv;
     const int R = probe_rows_per_wg(group, info->tile);
     const int64_t subtiles = info->tile / R;
-    if ((int64_t)info->n_items * subtiles * hkv > INT32_MAX)
+    const int nw = group * R / 32;
+    const ProbeSplit split = probe_split(nw, subtiles * hkv, info);
+    const int64_t slots = split.slots;
+    if (slots * subtiles * hkv > INT32_MAX)
         return fail(TA_ERR_UNSUPPORTED, "%s: grid too large", fn);
+    // per-lane copy offsets use 24-bit multiplies of the K/V row pitch
+    if (2LL * hkv * head_dim >= (1LL << 24))
+        return fail(TA_ERR_UNSUPPORTED, "%s: hkv * head_dim too large", fn);
 
     double *part = static_cast<double *>(workspace);
     if (info->n_items > 0) {
@@ -421,15 +686,17 @@ extern "C" ta_status region_grad_probe(const void *q, const void *k, const void 
         a.window = window;
         a.last = last;
         a.scale_log2 = softmax_scale * kProbeLog2e;
-        const int nw = group * R / 32;
-        dim3 grid((unsigned)((int64_t)info->n_items * subtiles * hkv));
+        a.n_slots = (int32_t)slots;
+        a.per_item = split.per_item ? 1 : 0;
+        a.total_cost = info->kept_tiles_per_qhead;
+        dim3 grid((unsigned)(slots * subtiles * hkv));
         hipError_t err = head_dim == 128 ? launch_probe<128>(nw, grid, a, stream)
                                          : launch_probe<64>(nw, grid, a, stream);
         if (err != hipSuccess)
             return fail(TA_ERR_HIP, "%s: probe kernel launch failed: %s", fn,
                         hipGetErrorString(err));
     }
-    const int64_t n_blocks = info->n_items > 0 ? (int64_t)info->n_items * (info->tile / 32) : 0;
+    const int64_t n_blocks = info->n_items > 0 ? slots * (info->tile / 32) : 0;
     hipLaunchKernelGGL(probe_reduce_kernel, dim3((unsigned)(hq * 3)), dim3(256), 0, stream,
                        part, n_blocks, hq * 3, region_sums);
     hipError_t err = hipGetLastError();

@@ -3,6 +3,7 @@ the sections of Appendix A.3) through the C interface, against the fp64
 oracle on the same seeded Q, K, V, dO and the same fp32 row normalisers
 (taken from the oracle's causal LSE, rounded to fp32)."""
 import math
+import os
 
 import numpy as np
 import pytest
@@ -23,8 +24,9 @@ pytestmark = pytest.mark.gpu
 REL_ABS = 5e-5
 
 
-def _probe(q, k, v, dout, lse, cu, tile, S, W, L, scale):
-    plan = B.Plan("causal", cu, 0, 1, 0, tile, q.shape[1], q.shape[2], device=q.device)
+def _probe(q, k, v, dout, lse, cu, tile, S, W, L, scale, plan=None):
+    if plan is None:
+        plan = B.Plan("causal", cu, 0, 1, 0, tile, q.shape[1], q.shape[2], device=q.device)
     nbytes = B.ta_probe_workspace_bytes(plan.info, q.shape[1])
     ws = torch.full((max(nbytes, 1),), 0xFF, dtype=torch.uint8, device=q.device)
     sums = torch.full((q.shape[1], 3), float("nan"), dtype=torch.float64, device=q.device)
@@ -68,6 +70,49 @@ CASES = [
 @pytest.mark.parametrize("cu,hq,hkv,d,tile,S,W,L", CASES)
 def test_probe_parity(cu, hq, hkv, d, tile, S, W, L):
     _check(cu, hq, hkv, d, tile, S, W, L, len(cu) + hq + d + S)
+
+
+@pytest.mark.parametrize("cu,hq,hkv,d,tile,S,W,L", [
+    ([0, 0, 333, 900, 901], 28, 4, 128, 64, 4, 40, 30),
+    ([0, 2048], 32, 8, 128, 128, 64, 128, 128),
+])
+def test_probe_shares(cu, hq, hkv, d, tile, S, W, L):
+    """Any number of equal shares (one slot: each workgroup walks every item;
+    more slots than k-tiles: most shares empty) gives the oracle's sums; the
+    shares cut items at k-tile boundaries, so the sums differ only in fp64
+    summation order between slot counts."""
+    runs = {}
+    try:
+        for slots in (1, 3, 16, 512):
+            os.environ["TRIATTN_PROBE_SLOTS"] = str(slots)
+            log(f"  slots {slots}")
+            runs[slots], _ = _check(cu, hq, hkv, d, tile, S, W, L, 77)
+    finally:
+        os.environ.pop("TRIATTN_PROBE_SLOTS", None)
+    ref = runs[1]
+    for slots, got in runs.items():
+        assert np.allclose(got, ref, rtol=1e-12, atol=1e-15), slots
+
+
+def test_probe_corrupt_schedule_gives_nan():
+    cu, hq, hkv, d = [0, 900], 8, 2, 128
+    q, k, v = (t.cuda() for t in draw_qkv(cu, hq, hkv, d, 9))
+    dout = draw_dout(cu, hq, d, 10).cuda()
+    lse = torch.zeros((hq, cu[-1]), dtype=torch.float32, device="cuda")
+    plan = B.Plan("causal", cu, 0, 1, 0, 128, hq, d, device="cuda")
+    good = plan.sched.clone()
+    got, _ = _probe(q, k, v, dout, lse, cu, 128, 16, 64, 32, 0.1, plan)
+    assert np.all(np.isfinite(got))
+    item = B.HDR_WORDS + B.ITEM_WORDS * (plan.info.n_items - 1)
+    for word, value, what in ((0, int(good[0]) ^ 1, "magic"),
+                              (item + 10, int(good[item + 10]) + 1, "cost"),
+                              (item + 5, 1 << 20, "ka1 past the sequence"),
+                              (item + 3, 1 << 20, "r1 past the sequence")):
+        plan.sched.copy_(good)
+        plan.sched[word] = value
+        got, _ = _probe(q, k, v, dout, lse, cu, 128, 16, 64, 32, 0.1, plan)
+        assert np.isnan(got).any(), what
+        log(f"corrupt probe schedule ({what}): NaN sums")
 
 
 def test_probe_paper_shape():

@@ -163,7 +163,9 @@ def test_probe_rejects_bad_arguments_without_launching():
     _, cau = B.ta_build_schedule("causal", [0, 100], 0, 1, 0, 64)
     _, tri = B.ta_build_schedule("triangle", [0, 100], 4, 8, 2, 64)
     ws = B.ta_probe_workspace_bytes(cau, 8)
-    assert ws == cau.n_items * 2 * 8 * 3 * 8
+    # one fp64 partial per (slot, 32-row block, head, section), at most 512
+    # slots per (kv head, row block)
+    assert ws == 512 * 2 * 8 * 3 * 8
 
     def call(info=cau, total=100, hq=8, hkv=2, d=128, scale=0.1, S=4, W=8, L=2,
              sums=FAKE, ws_ptr=FAKE, ws_bytes=ws, ptr=FAKE):
