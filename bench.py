@@ -61,7 +61,8 @@ def kernel_source_hash(texts=None) -> str:
     the files' current contents."""
     h = hashlib.sha256()
     rels = ("paper_2507_21526_amd/csrc/triattn_fwd.hip",
-            "paper_2507_21526_amd/csrc/triattn_internal.h")
+            "paper_2507_21526_amd/csrc/triattn_internal.h",
+            "paper_2507_21526_amd/csrc/triattn_device.h")
     for i, rel in enumerate(rels):
         if texts is not None:
             text = texts[i]
@@ -175,11 +176,12 @@ def summarize(root, workload):
                     tail = v[1:] or v
                 out.write(f"| {k} | {wgs} | {len(v)} | {sum(v) / len(v):.4f} | "
                           f"{min(v):.4f} | {sum(tail) / len(tail):.4f} |\n")
-            out.write("\nFor llama8b_n128k the Triangle tile pass launches "
-                      "(57 Last splits + 1023 streaming q-tiles) x 2 row halves x "
-                      "8 kv heads = 17280 workgroups; dense causal launches "
-                      "1024 x 2 x 8 = 16384; the merge launches 128 rows x 32 "
-                      "heads / 4 = 1024.\n")
+            if workload == "llama8b_n128k":
+                out.write("\nFor llama8b_n128k the Triangle tile pass launches "
+                          "(57 Last splits + 1023 streaming q-tiles) x 2 row halves x "
+                          "8 kv heads = 17280 workgroups; dense causal launches "
+                          "1024 x 2 x 8 = 16384; the merge launches 128 rows x 32 "
+                          "heads / 4 = 1024.\n")
     fetch = _pmc_per_kernel(os.path.join(root, "fetch"), "FETCH_SIZE")
     write = _pmc_per_kernel(os.path.join(root, "write"), "WRITE_SIZE")
     if fetch and write:
@@ -221,8 +223,93 @@ def summarize(root, workload):
         }
         with open(os.path.join(prof, f"traffic_tile_kernel_{workload}.json"), "w") as out:
             json.dump(rec, out, indent=1)
+    counters = summarize_counters(root, workload)
     print(json.dumps({"summarized": root, "trace": bool(stats),
-                      "traffic": bool(fetch and write)}))
+                      "traffic": bool(fetch and write), "counters": counters}))
+
+
+COUNTER_SETS = (
+    ("sqa", "SQ_INSTS_MFMA SQ_INSTS_VALU SQ_INSTS_LDS SQ_INSTS_SALU SQ_INSTS_VALU_TRANS_F32 "
+            "SQ_LDS_BANK_CONFLICT SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES", ""),
+    ("sqb", "GRBM_GUI_ACTIVE SQ_WAVES SQ_CYCLES SQ_WAVE_CYCLES SQ_ACTIVE_INST_VALU "
+            "SQ_ACTIVE_INST_LDS SQ_WAIT_INST_LDS SQ_INSTS_VMEM_RD", "--kernel-trace "),
+)
+
+
+def summarize_counters(root, workload):
+    """profiles/counters_tile_kernel_<workload>.md from two rocprofv3 --pmc
+    passes over the Triangle step (root/sqa, root/sqb: COUNTER_SETS), the
+    second with --kernel-trace for the launch durations.  Values are those
+    of the last Triangle tile launch of each pass."""
+    import csv
+    import glob
+    vals, dur_ms, wgs = {}, None, None
+    for sub, _, _ in COUNTER_SETS:
+        per = {}
+        for f in glob.glob(os.path.join(root, sub, "**", "*counter_collection.csv"),
+                           recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    if TILE_KERNEL not in r["Kernel_Name"]:
+                        continue
+                    key = int(r["Dispatch_Id"])
+                    d = per.setdefault(key, {})
+                    d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(
+                        r["Counter_Value"])
+                    d["_grid"] = int(r.get("Grid_Size", 0) or 0) // max(
+                        int(r.get("Workgroup_Size", 1) or 1), 1)
+        if not per:
+            return False
+        # the Triangle pass has the largest grid of the step's tile launches
+        grid = max(d["_grid"] for d in per.values())
+        last = max(k for k, d in per.items() if d["_grid"] == grid)
+        vals.update({k: v for k, v in per[last].items() if not k.startswith("_")})
+        wgs = grid
+        if sub == "sqb":
+            for f in glob.glob(os.path.join(root, sub, "**", "*kernel_trace.csv"),
+                               recursive=True):
+                with open(f) as fh:
+                    for r in csv.DictReader(fh):
+                        if int(r["Dispatch_Id"]) == last:
+                            dur_ms = (int(r["End_Timestamp"]) -
+                                      int(r["Start_Timestamp"])) / 1e6
+    mfma = vals["SQ_INSTS_MFMA"]
+    busy = vals["SQ_VALU_MFMA_BUSY_CYCLES"]
+    cyc_xcd = vals["GRBM_GUI_ACTIVE"] / 8.0
+    util = busy / (1024.0 * cyc_xcd)
+    ghz = cyc_xcd / (dur_ms * 1e6) if dur_ms else None
+    path = os.path.join(ROOT, "profiles", f"counters_tile_kernel_{workload}.md")
+    with open(path, "w") as out:
+        out.write(f"# rocprofv3 counters, attn_tile_kernel, Triangle pass of {workload} "
+                  f"({wgs} workgroups)\n\n")
+        out.write(f"Kernel source hash {kernel_source_hash()} (comment-blind, as in "
+                  "bench.py). Two passes, one counter set each, from the repository "
+                  "root on one MI355X:\n\n")
+        for sub, ctrs, extra in COUNTER_SETS:
+            out.write(f"    rocprofv3 --pmc {ctrs} {extra}--output-format csv -d <dir>/{sub} "
+                      f"-- python3 bench.py --workload {workload} --steps 2 --warmup 1 "
+                      "--no-dense --no-cpu-baseline --no-extra\n")
+        out.write("\nValues of the last Triangle tile launch of each pass"
+                  + (f" (duration under counter collection {dur_ms:.3f} ms)" if dur_ms else "")
+                  + ".\n\n| counter | value |\n|---|---|\n")
+        for k in sorted(vals):
+            out.write(f"| {k} | {vals[k]:.4e} |\n")
+        out.write("\nDerived:\n\n")
+        out.write(f"* MFMA instructions {mfma:.4e}; SQ_VALU_MFMA_BUSY_CYCLES / MFMA = "
+                  f"{busy / mfma:.1f} cycles each.\n")
+        out.write(f"* Cycles per XCD (GRBM_GUI_ACTIVE / 8) {cyc_xcd:.4e}; matrix-pipe "
+                  f"utilisation over the launch {util:.3f} (busy cycles / (1024 SIMDs x "
+                  "cycles))" + (f", at {ghz:.2f} GHz (cycles per XCD / duration)" if ghz else "")
+                  + ".\n")
+        out.write(f"* Per MFMA: VALU {vals['SQ_INSTS_VALU'] / mfma:.2f} (the count includes "
+                  f"the MFMAs), exp2 {vals['SQ_INSTS_VALU_TRANS_F32'] / mfma:.2f}, LDS "
+                  f"{vals['SQ_INSTS_LDS'] / mfma:.2f}, SALU {vals['SQ_INSTS_SALU'] / mfma:.2f}, "
+                  f"vector memory reads {vals['SQ_INSTS_VMEM_RD'] / mfma:.3f}.\n")
+        out.write(f"* LDS bank-conflict cycles {vals['SQ_LDS_BANK_CONFLICT']:.3e}, "
+                  f"{vals['SQ_LDS_BANK_CONFLICT'] / (256.0 * cyc_xcd) * 100:.2f} % of "
+                  "each CU's cycles; waves waiting on LDS: SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES = "
+                  f"{vals['SQ_WAIT_INST_LDS'] / vals['SQ_WAVE_CYCLES'] * 100:.1f} %.\n")
+    return True
 
 
 def cpu_model() -> str:

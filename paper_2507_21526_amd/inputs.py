@@ -69,6 +69,11 @@ WORKLOADS = {
         sink=128, window=4096, last=256, seed=1005, layers=28,
         triangle_layers=20,
         note="Qwen2.5-7B attention shape, 28 layers: 20 Triangle, 8 dense"),
+    "qwen7b_n128k_layer": Workload(
+        "qwen7b_n128k_layer", (0, 131072), hq=28, hkv=4, d=128, tile=128,
+        sink=128, window=4096, last=256, seed=1005,
+        note="one Triangle layer of the Qwen2.5-7B stack (GQA 7:1), for "
+             "per-layer timing and counters"),
     "triangle_n1m_g8": Workload(
         "triangle_n1m_g8", (0, 1048576), hq=8, hkv=1, d=128, tile=128,
         sink=128, window=2048, last=128, seed=1007,
