@@ -26,7 +26,7 @@ def test_kernel_hash_ignores_comments_only():
     other = "int f(int x) {\n  return x + 2;\n}\n"
     assert bench.code_text(src) == bench.code_text(same)
     assert bench.code_text(src) != bench.code_text(other)
-    assert bench.kernel_source_hash([src, ""]) == bench.kernel_source_hash([same, ""])
+    assert bench.kernel_source_hash([src, "", ""]) == bench.kernel_source_hash([same, "", ""])
 
 
 def test_element_exact_flops_count_the_kept_pairs():
