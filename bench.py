@@ -389,9 +389,11 @@ def time_loop(fn_steps, steps, warmup, torch):
 
 
 def gpu_qkv(total, hq, hkv, d, seed, dev, torch):
-    """Seeded N(0, 1) bf16 Q/K/V drawn on the device (timing sections only:
-    the run time does not depend on the values, and drawing 128K-token
-    layers on the host would dominate the run)."""
+    """Seeded N(0, 1) bf16 Q/K/V drawn on the device, for timing sections
+    whose workloads draw plain N(0, 1) values (no per-head scales or boosted
+    keys, so the logit range that the lazy re-base depends on is the
+    workload's own): drawing 128K-token layers on the host would dominate
+    the run."""
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
     out = []
