@@ -191,6 +191,41 @@ __device__ __forceinline__ int vswz(int r)
     return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
 }
 
+// Trim an item's two runs of 64-key steps, [a_lo, a_hi) then [b_lo, b_hi),
+// to the rows [wr0, wr_last] of one workgroup: steps whose keys all lie past
+// its last row (causal), or, for streaming rows, outside the sink and before
+// the window of its first row hold no kept pair and are skipped (their
+// scores would all be masked, so the result is the same bit for bit).  The
+// steps kept for streaming rows are those with a sink key, ceil(S / 64) from
+// key 0, and those from the window start of the first row on.
+__device__ __forceinline__ void trim_runs(bool stream, int sink, int window, int wr0,
+                                          int wr_last, int &a_lo, int &a_hi, int &b_lo,
+                                          int &b_hi)
+{
+    if (stream) {
+        const int first = wr0 - window + 1;
+        const int fs = first > 0 ? first / kStep : 0;  // first step with a window key
+        const int ss = (sink + kStep - 1) / kStep;     // steps with a sink key
+        if (b_hi > b_lo) {
+            // run a holds the sink k-tiles, run b the band
+            b_lo = min(max(b_lo, fs), b_hi);
+            a_hi = max(min(a_hi, ss), a_lo);
+        } else if (sink == 0) {
+            a_lo = min(max(a_lo, fs), a_hi);
+        } else if (fs > ss) {
+            // one run holds the sink and the band: split off the keys between
+            b_lo = min(fs, a_hi);
+            b_hi = a_hi;
+            a_hi = max(min(a_hi, ss), a_lo);
+        }
+    }
+    const int ls = wr_last / kStep + 1;  // first step past the last row
+    if (b_hi > b_lo)
+        b_hi = max(min(b_hi, ls), b_lo);
+    else
+        a_hi = max(min(a_hi, ls), a_lo);
+}
+
 // COPIER: the last of the NW waves only copies K/V tiles into LDS (all of
 // them, at the start of each matrix phase of group 0) and computes nothing;
 // the other NW - 1 waves compute.  For GQA group 7 (seven waves of 32 rows),
@@ -296,28 +331,13 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
 
     // Steps of 64 keys over the kept k-tiles: two runs, or a list (each
     // listed index clamped to the sequence's k-tiles).  The runs are trimmed
-    // to this workgroup's rows: steps whose keys all lie past its last row
-    // (causal), or, for streaming rows, before the window of its first row
-    // and outside the sink, hold no kept pair and are skipped.
+    // to this workgroup's rows (trim_runs).
     const int tps = a.tile / kStep;
     const int wr_last = min(wr0 + a.rows_per_wg, r1) - 1;
     int a_lo = ka0 * tps, a_hi = ka1 * tps, b_lo = kb0 * tps, b_hi = kb1 * tps;
-    if (!list_mode) {
-        if (mode == kModeStreaming) {
-            // run b (and run a when there is no sink) holds band keys only
-            const int first = wr0 - a.window + 1;
-            const int fs = first > 0 ? first / kStep : 0;
-            if (b_hi > b_lo)
-                b_lo = min(max(b_lo, fs), b_hi);
-            else if (a.sink == 0)
-                a_lo = min(max(a_lo, fs), a_hi);
-        }
-        const int ls = wr_last / kStep + 1;  // first step past the last row
-        if (b_hi > b_lo)
-            b_hi = max(min(b_hi, ls), b_lo);
-        else
-            a_hi = max(min(a_hi, ls), a_lo);
-    }
+    if (!list_mode)
+        trim_runs(mode == kModeStreaming, a.sink, a.window, wr0, wr_last, a_lo, a_hi, b_lo,
+                  b_hi);
     const int na = list_mode ? ka1 * tps : a_hi - a_lo;
     int nsteps = list_mode ? na : na + (b_hi - b_lo);
     // A list item's step keys are read from the list once, into an LDS
@@ -1204,19 +1224,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         const bool stream = mode == kModeStreaming;
         int a_lo = ka0 * tps, a_hi = ka1 * tps, b_lo = kb0 * tps, b_hi = kb1 * tps;
         const int wr_last = min(wr0 + a.rows_per_wg, r1) - 1;
-        if (stream) {
-            const int first = wr0 - a.window + 1;
-            const int fs = first > 0 ? first / kStep : 0;
-            if (b_hi > b_lo)
-                b_lo = min(max(b_lo, fs), b_hi);
-            else if (a.sink == 0)
-                a_lo = min(max(a_lo, fs), a_hi);
-        }
-        const int ls = wr_last / kStep + 1;
-        if (b_hi > b_lo)
-            b_hi = max(min(b_hi, ls), b_lo);
-        else
-            a_hi = max(min(a_hi, ls), a_lo);
+        trim_runs(stream, a.sink, a.window, wr0, wr_last, a_lo, a_hi, b_lo, b_hi);
         const int na = a_hi - a_lo;
         const int n = na + (b_hi - b_lo);
         const int rec[kUnitWords] = {n_total, n, seq_off, seq_len, wr0, r1, part_base,
