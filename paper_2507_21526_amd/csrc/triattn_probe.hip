@@ -129,19 +129,23 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
     const bool copy_wave = wave < N_COPY_WAVES;
 
     const int32_t *sched = a.sched;
+    // The item words are read without waiting for the header check, so that
+    // both loads are in flight together (the host has checked that the
+    // schedule holds n_items items, so the reads are in bounds either way).
     bool ok = probe_header_ok(sched, a.total_tokens, a.n_items, a.tile, a.total_cost);
     // The workgroup's share of kept k-tiles [lo, hi), counted over the items
     // laid end to end in schedule order from `pre` at item `item`: one whole
     // item (per-item launch), or an equal share of the total.
     int item = 0;
     int64_t pre = 0, lo = 0, hi = 0;
-    if (ok && a.per_item) {
+    if (a.per_item) {
         item = slot;
         hi = sched[kHdrWords + (int64_t)item * kItemWords + I_COST];
-    } else if (ok) {
+    } else {
         const int64_t per = (a.total_cost + a.n_slots - 1) / a.n_slots;
         lo = min((int64_t)slot * per, a.total_cost);
         hi = min(lo + per, a.total_cost);
+        pre = lo;  // an empty share is covered as it stands
         if (lo < hi) {
             // Item holding k-tile lo: thread t sums the costs of items
             // [t m, t m + m), a scan over the threads gives each its prefix,
@@ -184,7 +188,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
                 }
                 p += c;
             }
-            ok = !__syncthreads_or(neg) && total == a.total_cost && first[0] >= 0;
+            const bool any_neg = __syncthreads_or(neg);
+            ok = ok && !any_neg && total == a.total_cost && first[0] >= 0;
             item = __builtin_amdgcn_readfirstlane((int)first[0]);
             pre = first[1];
         }
@@ -500,36 +505,29 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
 }
 
 // out[hr] = sum over blocks b of part[b, hr] (hr = head * 3 + section), in a
-// fixed order: thread-strided sums, then a tree over the workgroup.
+// fixed order: one wave per output, lane-strided sums, then an xor-shuffle
+// tree.  Four outputs per workgroup.
 __global__ __launch_bounds__(256) void probe_reduce_kernel(const double *part, int64_t n_blocks,
                                                            int32_t hq3, double *out)
 {
-    __shared__ double red[256];
-    const int hr = blockIdx.x;
+    const int hr = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (hr >= hq3)
+        return;
+    const int lane = threadIdx.x & 63;
     double s = 0.0;
-    for (int64_t b = threadIdx.x; b < n_blocks; b += 256)
+    for (int64_t b = lane; b < n_blocks; b += 64)
         s += part[b * hq3 + hr];
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w)
-            red[threadIdx.x] += red[threadIdx.x + w];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0)
-        out[hr] = red[0];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        s += __shfl_xor(s, off);
+    if (lane == 0)
+        out[hr] = s;
 }
 
 int probe_rows_per_wg(int group, int tile)
 {
-    int max_waves = 8;
-    if (const char *env = std::getenv("TRIATTN_PROBE_WAVES")) {
-        const long forced = std::strtol(env, nullptr, 10);
-        if (forced >= 1 && forced <= 8)
-            max_waves = (int)forced;
-    }
     for (int r = 128; r >= 32; r /= 2)
-        if (r <= tile && group * r / 32 <= max_waves)
+        if (r <= tile && group * r / 32 <= 8)
             return r;
     return 32;
 }
@@ -697,8 +695,8 @@ extern "C" ta_status region_grad_probe(const void *q, const void *k, const void 
                         hipGetErrorString(err));
     }
     const int64_t n_blocks = info->n_items > 0 ? slots * (info->tile / 32) : 0;
-    hipLaunchKernelGGL(probe_reduce_kernel, dim3((unsigned)(hq * 3)), dim3(256), 0, stream,
-                       part, n_blocks, hq * 3, region_sums);
+    hipLaunchKernelGGL(probe_reduce_kernel, dim3((unsigned)((hq * 3 + 3) / 4)), dim3(256), 0,
+                       stream, part, n_blocks, hq * 3, region_sums);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess)
         return fail(TA_ERR_HIP, "%s: reduce kernel launch failed: %s", fn,
