@@ -54,6 +54,8 @@ EDGE = [
     ([0, 37], 2, 1, 128, 4, 8, 5, 64),
     ([0, 200], 7, 1, 128, 8, 64, 24, 64),          # G = 7
     ([0, 300], 28, 4, 128, 16, 100, 40, 128),      # Qwen group shape
+    ([0, 33, 450], 14, 2, 64, 8, 96, 40, 128),     # G = 7, d 64 (copier wave)
+    ([0, 700], 7, 1, 128, 8, 256, 128, 128),       # G = 7, sink tile split around the window
     ([0, 513], 4, 4, 64, 0, 70, 0, 64),            # streaming only, no sink
     ([0, 640], 8, 2, 128, 130, 65, 129, 128),      # sink not tile aligned
     ([0, 0, 100, 100, 357, 1000], 4, 2, 64, 3, 50, 77, 64),  # varlen + empty

@@ -81,11 +81,16 @@ def test_llama_varlen():
 
 
 def test_qwen_stack_layers():
+    # six of the 28 layers, each with its own seeded inputs: the first,
+    # middle and last of the Triangle set and of the dense set (GQA 7:1, the
+    # seven-compute-wave layout with a copier wave)
     w = WORKLOADS["qwen7b_n128k_stack28"]
     tri = triangle_layer_set(w)
     dense = [l for l in range(w.layers) if l not in tri]
-    _check_workload("qwen7b_n128k_stack28", tri[0], kinds=("triangle",))
-    _check_workload("qwen7b_n128k_stack28", dense[0], kinds=("causal",))
+    for layer in (tri[0], tri[len(tri) // 2], tri[-1]):
+        _check_workload("qwen7b_n128k_stack28", layer, kinds=("triangle",), n_random=48)
+    for layer in (dense[0], dense[len(dense) // 2], dense[-1]):
+        _check_workload("qwen7b_n128k_stack28", layer, kinds=("causal",), n_random=48)
 
 
 def test_mha_32k():
