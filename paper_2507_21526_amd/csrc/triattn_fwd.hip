@@ -586,6 +586,18 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         const bool stream_mode = mode == kModeStreaming;
         const int sink_lim = stream_mode ? a.sink - key0 - 8 * half : kStep;
         const int win_lim = stream_mode ? lim - a.window : -1;
+        if (stream_mode && key0 + kStep - 1 <= row_base - a.window) {
+            // a step before every row's window (and before its diagonal):
+            // only its sink keys are kept
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int off = kb * 32 + key_of_reg(v, 0);
+                    sacc[kb][v] = off < sink_lim ? sacc[kb][v] : -INFINITY;
+                }
+            return;
+        }
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -1448,6 +1460,17 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         }
         const int win_lim = lim - a.window;             // offset > win_lim: in the window
         const int sink_lim = a.sink - key0 - 8 * half;  // offset < sink_lim: a sink key
+        if (key0 + kStep - 1 <= cur_row_base - a.window) {
+            // before every row's window (and diagonal): only sink keys remain
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int off = kb * 32 + key_of_reg(v, 0);
+                    sacc[kb][v] = keep_if(sacc[kb][v], (off - sink_lim) >> 31);
+                }
+            return;
+        }
         if (!need_causal && key0 >= a.sink) {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
