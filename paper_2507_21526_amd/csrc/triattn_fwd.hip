@@ -226,6 +226,28 @@ __device__ __forceinline__ void trim_runs(bool stream, int sink, int window, int
         a_hi = max(min(a_hi, ls), a_lo);
 }
 
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f)
+{
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// LDS reads that MFMAs i .. i + count - 1 of a matrix phase need: one K
+// fragment for each of the first NQ MFMAs (none for the first KPRE ones when
+// they were read ahead), two transposed V reads for each later one.
+template <int NQ, int N, int KPRE, bool PRE>
+constexpr int phase_reads(int i, int count)
+{
+    int r = 0;
+    for (int m = i; m < i + count && m < N; ++m)
+        r += m >= NQ ? 2 : (PRE && m < KPRE) ? 0 : 1;
+    return r;
+}
+
 // COPIER: the last of the NW waves only copies K/V tiles into LDS (all of
 // them, at the start of each matrix phase of group 0) and computes nothing;
 // the other NW - 1 waves compute.  For GQA group 7 (seven waves of 32 rows),
@@ -500,29 +522,60 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
 #pragma unroll
     for (int s = 0; s < QK_STEPS; ++s)
         koff[s] = (uint32_t)(krow0 * ROW_BYTES + (((2 * s + half) ^ kswz<D>(krow0)) << 4));
-    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) TA_INLINE {
+    // The first KPRE K fragments of a matrix phase can be read ahead, in the
+    // wave's softmax phase before it, when the stage has landed by then: the
+    // first MFMAs of the phase then wait for no LDS read.
+    constexpr int KPRE = 2 * QK_STEPS < 6 ? 2 * QK_STEPS : 6;
+    bf16x8 kpre[KPRE];
+    auto prefetch_k = [&](int buf) TA_INLINE {
+        const unsigned char *kt = smem + buf * STAGE_BYTES;
+#pragma unroll
+        for (int i = 0; i < KPRE; ++i)
+            kpre[i] = *reinterpret_cast<const bf16x8 *>(kt + koff[i / 2] +
+                                                          (i & 1) * 32 * ROW_BYTES);
+    };
+    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook, auto pre, auto own) TA_INLINE {
+        constexpr bool PRE = decltype(pre)::value;
         const unsigned char *kt = smem + buf * STAGE_BYTES;
         sacc[0] = f32x16{};
         sacc[1] = f32x16{};
 #pragma unroll
         for (int s = 0; s < QK_STEPS; ++s) {
-            const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(kt + koff[s]);
-            const bf16x8 a1 =
-                *reinterpret_cast<const bf16x8 *>(kt + koff[s] + 32 * ROW_BYTES);
+            bf16x8 a0, a1;
+            if (PRE && 2 * s + 1 < KPRE) {
+                a0 = kpre[2 * s];
+                a1 = kpre[2 * s + 1];
+            } else {
+                a0 = *reinterpret_cast<const bf16x8 *>(kt + koff[s]);
+                a1 = *reinterpret_cast<const bf16x8 *>(kt + koff[s] + 32 * ROW_BYTES);
+            }
             sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[s], sacc[0], 0, 0, 0);
             hook(2 * s);
             sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[s], sacc[1], 0, 0, 0);
             hook(2 * s + 1);
         }
-        // keep six operand reads in flight ahead of the MFMAs
         constexpr int n = 2 * QK_STEPS, ahead = 6;
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
+        if constexpr (!decltype(own)::value) {
+            // the caller schedules the reads of the whole phase
+        } else if constexpr (PRE) {
+            // read r feeds MFMA KPRE + r: one read before each MFMA from the
+            // first keeps them KPRE MFMAs ahead
 #pragma unroll
-        for (int i = 0; i < n - ahead; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            for (int i = 0; i < n - KPRE; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, KPRE, 0);
+        } else {
+            // keep six operand reads in flight ahead of the MFMAs
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
+#pragma unroll
+            for (int i = 0; i < n - ahead; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
     };
 
     f32x16 oacc[D_BLOCKS];
@@ -546,7 +599,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         voff[b] = (uint32_t)(vrow0 * ROW_BYTES + (((d >> 3) ^ vswz<D>(vrow0)) << 4) +
                              (d & 7) * 2);
     }
-    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) TA_INLINE {
+    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook, auto own) TA_INLINE {
         const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -568,14 +621,34 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                     hook(2 * QK_STEPS + (kb * 2 + s2) * D_BLOCKS + b);
                 }
         // two transposed reads per MFMA; keep four MFMAs' operands in flight
-        constexpr int n = 4 * D_BLOCKS, ahead = 4;
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * ahead, 0);
+        if constexpr (decltype(own)::value) {
+            constexpr int n = 4 * D_BLOCKS, ahead = 4;
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * ahead, 0);
 #pragma unroll
-        for (int i = 0; i < n - ahead; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+            for (int i = 0; i < n - ahead; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
+    };
+    // Reads of a whole matrix phase (QK^T then PV) in one sequence: MFMA i
+    // needs one K read (i < NQ, none for prefetched fragments) or two V
+    // reads; the reads of MFMA i + ahead are issued just before MFMA i, so
+    // the first V reads overlap the last QK^T MFMAs instead of waiting for
+    // them to issue.
+    auto sched_phase = [&](auto pre) TA_INLINE {
+        constexpr bool PRE = decltype(pre)::value;
+        constexpr int NQ = 2 * QK_STEPS, N = NQ + 4 * D_BLOCKS, ahead = 6;
+        constexpr int first = phase_reads<NQ, N, KPRE, PRE>(0, ahead);
+        if constexpr (first > 0)
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, first, 0);
+        static_for<0, N>([&](auto ic) TA_INLINE {
+            constexpr int nr = phase_reads<NQ, N, KPRE, PRE>(decltype(ic)::value + ahead, 1);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            if constexpr (nr > 0)
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, nr, 0);
+        });
     };
 
     // Element mask (branch-free selects) where the step crosses the diagonal
@@ -691,15 +764,21 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // Inside the step loops (unrolled by two) the LDS stage is a
     // std::integral_constant, so every LDS operand address is a per-lane
     // offset plus an immediate.
-    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook) TA_INLINE {
+    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook, auto pre) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(1);  // MFMA issue goes first on the SIMD
         __builtin_amdgcn_sched_barrier(0);
         const int buf = stage;
-        if (has_qk)
-            qk(buf, s_acc, hook);
-        if (has_pv)
-            pv(buf, p_acc, hook);
+        if (!COPIER && has_qk && has_pv) {
+            qk(buf, s_acc, hook, pre, std::false_type{});
+            pv(buf, p_acc, hook, std::false_type{});
+            sched_phase(pre);
+        } else {
+            if (has_qk)
+                qk(buf, s_acc, hook, pre, std::true_type{});
+            if (has_pv)
+                pv(buf, p_acc, hook, std::true_type{});
+        }
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(0);
         __builtin_amdgcn_sched_barrier(0);
@@ -779,7 +858,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             // j = 0: QK only, then the copies of the PV slots.
             if constexpr (!COPIER)
                 plan_step_copies(0, Stage0{});
-            do_m(Stage0{}, true, false, g0_hook);
+            do_m(Stage0{}, true, false, g0_hook, std::false_type{});
             if constexpr (!COPIER) {
 #pragma unroll
                 for (int c = 0; c < 2 * COPIES; ++c)
@@ -793,7 +872,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             auto step = [&](int j, auto stage) TA_INLINE {
                 if constexpr (!COPIER)
                     plan_step_copies(j, stage);
-                do_m(stage, true, true, g0_hook);
+                do_m(stage, true, true, g0_hook, std::false_type{});
                 end_phase(false);
                 do_x(j);
                 end_phase(true);
@@ -805,17 +884,26 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             }
             if (j < nsteps)
                 step(j, Stage1{});
-            do_m(nsteps & 1, false, true, no_hook);
+            do_m(nsteps & 1, false, true, no_hook, std::false_type{});
             end_phase(false);
             end_phase(false);
         } else {
+            // Group 1's matrix phase M(j) reads stage j & 1, whose K(j) has
+            // landed before the phase in which group 1 runs X(j - 1): the
+            // first K fragments of M(j) are read at the start of that phase
+            // (not with a copier wave, where it measured slower).
+            constexpr bool PRE = !COPIER;
+            if constexpr (PRE)
+                prefetch_k(0);
             end_phase(false);
-            do_m(Stage0{}, true, false, no_hook);
+            do_m(Stage0{}, true, false, no_hook, std::bool_constant<PRE>{});
             end_phase(false);
             auto step = [&](int j, auto stage) TA_INLINE {
+                if constexpr (PRE)
+                    prefetch_k(stage);
                 do_x(j - 1);
                 end_phase(false);
-                do_m(stage, true, true, no_hook);
+                do_m(stage, true, true, no_hook, std::bool_constant<PRE>{});
                 end_phase(false);
             };
             int j = 1;
@@ -827,7 +915,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 step(j, Stage1{});
             do_x(nsteps - 1);
             end_phase(false);
-            do_m(nsteps & 1, false, true, no_hook);
+            do_m(nsteps & 1, false, true, no_hook, std::false_type{});
             end_phase(false);
         }
     } else {
