@@ -253,7 +253,9 @@ constexpr int phase_reads(int i, int count)
 // the other NW - 1 waves compute.  For GQA group 7 (seven waves of 32 rows),
 // whose eighth ping-pong slot would otherwise be empty: the MFMA waves then
 // issue no copies.
-template <int D, int NW, bool COPIER = false>
+// LIST: the kernel serves block-sparse schedules, whose list items read
+// their k-tiles from the schedule's list section (the other kinds have none).
+template <int D, int NW, bool COPIER = false, bool LIST = false>
 __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(FwdArgs a,
                                                                                int32_t kind)
 {
@@ -290,6 +292,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     constexpr int QREGION = Q_IN_STAGE ? STAGE_BYTES : N_STAGES * STAGE_BYTES;
     __shared__ __attribute__((aligned(1024))) unsigned char
         smem[N_STAGES * STAGE_BYTES + (Q_IN_STAGE ? 0 : NW * QTILE_BYTES)];
+    static_assert(sizeof(smem) + (LIST ? kKeyTable * 4 : 0) <= 160 * 1024, "LDS of a CU");
 
     const int32_t *sched = a.sched;
     int bid = blockIdx.x;
@@ -315,11 +318,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // Block-sparse schedules record the length of their k-tile lists.  List
     // items (kModeCausalList) read the k-tiles list[ka0 .. ka0 + ka1) of the
     // tile-list section instead of two runs.
-    const bool list_mode = mode == kModeCausalList;
+    const bool list_mode = LIST && mode == kModeCausalList;
     if (!header_ok(sched, a.total_tokens, a.n_items, kind) ||
         a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0) ||
         seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
         r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || kb0 < 0 || kb1 < kb0 ||
+        (!LIST && mode == kModeCausalList) ||
         (list_mode ? (ka1 < 0 || kb1 != kb0 || (int64_t)ka0 + ka1 > a.list_words)
                    : ka1 < ka0) ||
         (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows)) {
@@ -366,7 +370,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // table, so that no step waits on a global load (a global load's wait
     // would also wait for the K/V copies in flight).  Longer lists than the
     // table read the list at every step.
-    __shared__ int32_t keytab[kKeyTable];
+    typedef __attribute__((address_space(3))) int32_t lds_i32;
+    lds_i32 *keytab = nullptr;
+    if constexpr (LIST) {
+        __shared__ int32_t tab[kKeyTable];
+        keytab = (lds_i32 *)tab;
+    }
     const bool use_tab = list_mode && na <= kKeyTable;
     if (use_tab) {
         for (int s = threadIdx.x; s < na; s += NW * 64) {
@@ -764,10 +773,15 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // Inside the step loops (unrolled by two) the LDS stage is a
     // std::integral_constant, so every LDS operand address is a per-lane
     // offset plus an immediate.
-    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook, auto pre) TA_INLINE {
+    // prep() runs inside the phase, so that its scalar work (planning the
+    // phase's copies) can overlap the first LDS reads.
+    auto no_prep = []() {};
+    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook, auto pre,
+                    auto prep) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(1);  // MFMA issue goes first on the SIMD
         __builtin_amdgcn_sched_barrier(0);
+        prep();
         const int buf = stage;
         if (!COPIER && has_qk && has_pv) {
             qk(buf, s_acc, hook, pre, std::false_type{});
@@ -856,9 +870,11 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             end_phase(false);  // stage 1 is free once every wave has read its Q
         if (group == 0) {
             // j = 0: QK only, then the copies of the PV slots.
-            if constexpr (!COPIER)
-                plan_step_copies(0, Stage0{});
-            do_m(Stage0{}, true, false, g0_hook, std::false_type{});
+            auto prep0 = [&]() TA_INLINE {
+                if constexpr (!COPIER)
+                    plan_step_copies(0, Stage0{});
+            };
+            do_m(Stage0{}, true, false, g0_hook, std::false_type{}, prep0);
             if constexpr (!COPIER) {
 #pragma unroll
                 for (int c = 0; c < 2 * COPIES; ++c)
@@ -870,9 +886,11 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             end_phase(true);
             // step j reads stage j & 1 (odd j first)
             auto step = [&](int j, auto stage) TA_INLINE {
-                if constexpr (!COPIER)
-                    plan_step_copies(j, stage);
-                do_m(stage, true, true, g0_hook, std::false_type{});
+                auto prep = [&]() TA_INLINE {
+                    if constexpr (!COPIER)
+                        plan_step_copies(j, stage);
+                };
+                do_m(stage, true, true, g0_hook, std::false_type{}, prep);
                 end_phase(false);
                 do_x(j);
                 end_phase(true);
@@ -884,7 +902,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             }
             if (j < nsteps)
                 step(j, Stage1{});
-            do_m(nsteps & 1, false, true, no_hook, std::false_type{});
+            do_m(nsteps & 1, false, true, no_hook, std::false_type{}, no_prep);
             end_phase(false);
             end_phase(false);
         } else {
@@ -896,14 +914,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             if constexpr (PRE)
                 prefetch_k(0);
             end_phase(false);
-            do_m(Stage0{}, true, false, no_hook, std::bool_constant<PRE>{});
+            do_m(Stage0{}, true, false, no_hook, std::bool_constant<PRE>{}, no_prep);
             end_phase(false);
             auto step = [&](int j, auto stage) TA_INLINE {
                 if constexpr (PRE)
                     prefetch_k(stage);
                 do_x(j - 1);
                 end_phase(false);
-                do_m(stage, true, true, no_hook, std::bool_constant<PRE>{});
+                do_m(stage, true, true, no_hook, std::bool_constant<PRE>{}, no_prep);
                 end_phase(false);
             };
             int j = 1;
@@ -915,7 +933,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 step(j, Stage1{});
             do_x(nsteps - 1);
             end_phase(false);
-            do_m(nsteps & 1, false, true, no_hook, std::false_type{});
+            do_m(nsteps & 1, false, true, no_hook, std::false_type{}, no_prep);
             end_phase(false);
         }
     } else {
@@ -1942,20 +1960,28 @@ int rows_per_wg(int group, int tile)
     return 32;
 }
 
-template <int D>
-hipError_t launch_tile(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_t s)
+template <int D, bool LIST>
+hipError_t launch_tile_as(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_t s)
 {
     switch (nw) {
-    case 2: hipLaunchKernelGGL((attn_tile_kernel<D, 2>), grid, dim3(128), 0, s, a, kind); break;
-    case 4: hipLaunchKernelGGL((attn_tile_kernel<D, 4>), grid, dim3(256), 0, s, a, kind); break;
-    case 5: hipLaunchKernelGGL((attn_tile_kernel<D, 5>), grid, dim3(320), 0, s, a, kind); break;
-    case 6: hipLaunchKernelGGL((attn_tile_kernel<D, 6>), grid, dim3(384), 0, s, a, kind); break;
+    case 2: hipLaunchKernelGGL((attn_tile_kernel<D, 2, false, LIST>), grid, dim3(128), 0, s, a, kind); break;
+    case 4: hipLaunchKernelGGL((attn_tile_kernel<D, 4, false, LIST>), grid, dim3(256), 0, s, a, kind); break;
+    case 5: hipLaunchKernelGGL((attn_tile_kernel<D, 5, false, LIST>), grid, dim3(320), 0, s, a, kind); break;
+    case 6: hipLaunchKernelGGL((attn_tile_kernel<D, 6, false, LIST>), grid, dim3(384), 0, s, a, kind); break;
     // seven compute waves and a copier wave
-    case 7: hipLaunchKernelGGL((attn_tile_kernel<D, 8, true>), grid, dim3(512), 0, s, a, kind); break;
-    case 8: hipLaunchKernelGGL((attn_tile_kernel<D, 8>), grid, dim3(512), 0, s, a, kind); break;
+    case 7: hipLaunchKernelGGL((attn_tile_kernel<D, 8, true, LIST>), grid, dim3(512), 0, s, a, kind); break;
+    case 8: hipLaunchKernelGGL((attn_tile_kernel<D, 8, false, LIST>), grid, dim3(512), 0, s, a, kind); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+// Block-sparse schedules (list items) run the list form of the kernel.
+template <int D>
+hipError_t launch_tile(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream_t s)
+{
+    return kind == TA_KIND_BLOCKSPARSE ? launch_tile_as<D, true>(nw, grid, a, kind, s)
+                                       : launch_tile_as<D, false>(nw, grid, a, kind, s);
 }
 
 ta_status check_common(const char *fn, int want_kind, const void *q, const void *k,
