@@ -1456,7 +1456,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
 #pragma unroll
     for (int s = 0; s < QK_STEPS; ++s)
         koff[s] = (uint32_t)(krow0 * ROW_BYTES + (((2 * s + half) ^ kswz<D>(krow0)) << 4));
-    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook) TA_INLINE {
+    // (No K fragments are read ahead here, unlike the single-unit kernel:
+    // the unit loop has no registers to spare for them.)
+    constexpr int KPRE = 0;
+    auto qk = [&](int buf, f32x16 (&sacc)[2], auto hook, auto pre, auto own) TA_INLINE {
+        (void)pre;
         const unsigned char *kt = smem + buf * STAGE_BYTES;
         sacc[0] = f32x16{};
         sacc[1] = f32x16{};
@@ -1471,13 +1475,17 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
             hook(2 * s + 1);
         }
         constexpr int n = 2 * QK_STEPS, ahead = 6;
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
+        if constexpr (!decltype(own)::value) {
+            // the caller schedules the reads of the whole phase
+        } else {
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
 #pragma unroll
-        for (int i = 0; i < n - ahead; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            for (int i = 0; i < n - ahead; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
     };
     const int vrow0 = 8 * half + ((lane & 15) >> 2);
     const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -1488,7 +1496,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         voff[b] = (uint32_t)(vrow0 * ROW_BYTES + (((d >> 3) ^ vswz<D>(vrow0)) << 4) +
                              (d & 7) * 2);
     }
-    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook) TA_INLINE {
+    auto pv = [&](int buf, const bf16x8 (&pf)[2][2], auto hook, auto own) TA_INLINE {
         const unsigned char *vt = smem + buf * STAGE_BYTES + TILE_BYTES;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -1509,14 +1517,32 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
                                                                      oacc[b], 0, 0, 0);
                     hook(2 * QK_STEPS + (kb * 2 + s2) * D_BLOCKS + b);
                 }
-        constexpr int n = 4 * D_BLOCKS, ahead = 4;
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * ahead, 0);
+        if constexpr (decltype(own)::value) {
+            constexpr int n = 4 * D_BLOCKS, ahead = 4;
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * ahead, 0);
 #pragma unroll
-        for (int i = 0; i < n - ahead; ++i) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+            for (int i = 0; i < n - ahead; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
+    };
+    // Reads of a whole matrix phase in one sequence (as in the single-unit
+    // kernel): the reads of MFMA i + 6 are issued just before MFMA i.
+    auto sched_phase = [&](auto pre) TA_INLINE {
+        constexpr bool PRE = false;
+        (void)pre;
+        constexpr int NQ = 2 * QK_STEPS, N = NQ + 4 * D_BLOCKS, ahead = 6;
+        constexpr int first = phase_reads<NQ, N, KPRE, PRE>(0, ahead);
+        if constexpr (first > 0)
+            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, first, 0);
+        static_for<0, N>([&](auto ic) TA_INLINE {
+            constexpr int nr = phase_reads<NQ, N, KPRE, PRE>(decltype(ic)::value + ahead, 1);
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            if constexpr (nr > 0)
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, nr, 0);
+        });
     };
 
     // The current unit, as the mask needs it (uniform).
@@ -1665,15 +1691,26 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
     const int group = wave >= NW - n_group1 ? 1 : 0;
     f32x16 s_acc[2];
     bf16x8 p_acc[2][2];
-    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook) TA_INLINE {
+    // prep() runs inside the phase, so that its scalar work (planning the
+    // phase's copies) can overlap the first LDS reads.
+    auto no_prep = []() {};
+    auto do_m = [&](auto stage, bool has_qk, bool has_pv, auto hook, auto pre,
+                    auto prep) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(1);
         __builtin_amdgcn_sched_barrier(0);
+        prep();
         const int buf = stage;
-        if (has_qk)
-            qk(buf, s_acc, hook);
-        if (has_pv)
-            pv(buf, p_acc, hook);
+        if (has_qk && has_pv) {
+            qk(buf, s_acc, hook, pre, std::false_type{});
+            pv(buf, p_acc, hook, std::false_type{});
+            sched_phase(pre);
+        } else {
+            if (has_qk)
+                qk(buf, s_acc, hook, pre, std::true_type{});
+            if (has_pv)
+                pv(buf, p_acc, hook, std::true_type{});
+        }
         __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(0);
         __builtin_amdgcn_sched_barrier(0);
@@ -1738,8 +1775,8 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
     if (group == 0) {
         wk = srec(min(1, n_total - 1));
         wv = srec(0);
-        plan_step_copies(Stage0{});
-        do_m(Stage0{}, true, false, copy_hook);
+        do_m(Stage0{}, true, false, copy_hook, std::false_type{},
+             [&]() TA_INLINE { plan_step_copies(Stage0{}); });
 #pragma unroll
         for (int cidx = 0; cidx < 2 * COPIES; ++cidx)
             if (cidx * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
@@ -1762,8 +1799,8 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
             const bool bnd = j == next_start;
             if (bnd)
                 read_q();
-            plan_step_copies(stage);
-            do_m(stage, true, true, copy_hook);
+            do_m(stage, true, true, copy_hook, std::false_type{},
+                 [&]() TA_INLINE { plan_step_copies(stage); });
             end_phase(false);
             if (bnd)
                 boundary();
@@ -1777,13 +1814,13 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         }
         if (j < n_total)
             step(j++, Stage1{});
-        do_m(j & 1, false, true, no_hook);
+        do_m(j & 1, false, true, no_hook, std::false_type{}, no_prep);
         end_phase(false);
         end_phase(false);
     } else {
         end_phase(false);
         int nx = ((lds_i32 *)stab)[0];
-        do_m(Stage0{}, true, false, no_hook);
+        do_m(Stage0{}, true, false, no_hook, std::false_type{}, no_prep);
         end_phase(false);
         // the word of step j - 1 was read during the matrix phase before
         auto step = [&](int j, auto stage) TA_INLINE {
@@ -1797,7 +1834,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
                 read_q();
             }
             nx = ((lds_i32 *)stab)[j];
-            do_m(stage, true, true, no_hook);
+            do_m(stage, true, true, no_hook, std::false_type{}, no_prep);
             end_phase(false);
         };
         int j = 1;
@@ -1812,7 +1849,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         wx = (uint32_t)__builtin_amdgcn_readfirstlane(nx);
         do_x();
         end_phase(false);
-        do_m(j & 1, false, true, no_hook);
+        do_m(j & 1, false, true, no_hook, std::false_type{}, no_prep);
         end_phase(false);
     }
     epilogue(rec_cur, l_run, m_ref);
