@@ -320,12 +320,35 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
         // Matrix phase of step j from LDS stage `stage`: S^T = K Q^T and
         // dP^T = V dO^T for the two 32-key halves, the four accumulator
         // chains interleaved so that dependent MFMAs do not stall.
-        auto do_m = [&](auto stage, auto hook) TA_INLINE {
+        // The first KPRE operand fragments of a matrix phase (its first MFMAs'
+        // K and V reads, in MFMA order) can be read ahead in the wave's vector
+        // phase before it, when the stage has landed by then (group 1).
+        constexpr int KPRE = 6;
+        bf16x8 kpre[KPRE];
+        auto frag = [&](const uint8_t *kt, int i) TA_INLINE -> bf16x8 {
+            // read i of a matrix phase: s = i / 4; k0, v0, k1, v1
+            const uint8_t *base = (i & 1) ? kt + TILE_BYTES : kt;
+            return *reinterpret_cast<const bf16x8 *>(base + aoff[i / 4] +
+                                                     ((i >> 1) & 1) * 32 * ROW_BYTES);
+        };
+        auto prefetch = [&](int buf) TA_INLINE {
+            const uint8_t *kt = lds + buf * STAGE_BYTES;
+#pragma unroll
+            for (int i = 0; i < KPRE; ++i)
+                kpre[i] = frag(kt, i);
+        };
+        // Matrix phase of step j from LDS stage `stage`: S^T = K Q^T and
+        // dP^T = V dO^T for the two 32-key halves, the four accumulator
+        // chains interleaved so that dependent MFMAs do not stall.  prep()
+        // runs inside the phase, so that its scalar work (planning the
+        // phase's copies) overlaps the first LDS reads.
+        auto do_m = [&](auto stage, auto hook, auto pre, auto prep) TA_INLINE {
+            constexpr bool PRE = decltype(pre)::value;
             __builtin_amdgcn_sched_barrier(0);
             __builtin_amdgcn_s_setprio(1);  // MFMA issue goes first on the SIMD
             __builtin_amdgcn_sched_barrier(0);
+            prep();
             const uint8_t *kt = lds + (int)stage * STAGE_BYTES;
-            const uint8_t *vt = kt + TILE_BYTES;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 sacc[kb] = f32x16{};
@@ -333,30 +356,39 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             }
 #pragma unroll
             for (int s = 0; s < QK; ++s) {
-                const bf16x8 k0 = *reinterpret_cast<const bf16x8 *>(kt + aoff[s]);
-                const bf16x8 v0 = *reinterpret_cast<const bf16x8 *>(vt + aoff[s]);
-                const bf16x8 k1 =
-                    *reinterpret_cast<const bf16x8 *>(kt + aoff[s] + 32 * ROW_BYTES);
-                const bf16x8 v1 =
-                    *reinterpret_cast<const bf16x8 *>(vt + aoff[s] + 32 * ROW_BYTES);
-                sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[s], sacc[0], 0, 0, 0);
+                bf16x8 f[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    f[u] = (PRE && 4 * s + u < KPRE) ? kpre[4 * s + u] : frag(kt, 4 * s + u);
+                sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[0], qf[s], sacc[0], 0, 0, 0);
                 hook(4 * s);
-                gacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v0, df[s], gacc[0], 0, 0, 0);
+                gacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[1], df[s], gacc[0], 0, 0, 0);
                 hook(4 * s + 1);
-                sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[s], sacc[1], 0, 0, 0);
+                sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[2], qf[s], sacc[1], 0, 0, 0);
                 hook(4 * s + 2);
-                gacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v1, df[s], gacc[1], 0, 0, 0);
+                gacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[3], df[s], gacc[1], 0, 0, 0);
                 hook(4 * s + 3);
             }
-            // keep six operand reads in flight ahead of the MFMAs
             constexpr int n = MFMA_SLOTS, ahead = 6;
-            __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
+            if constexpr (PRE) {
+                // read r feeds MFMA KPRE + r: one read before each MFMA from
+                // the first keeps them KPRE MFMAs ahead
 #pragma unroll
-            for (int i = 0; i < n - ahead; ++i) {
-                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                for (int i = 0; i < n - KPRE; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, KPRE, 0);
+            } else {
+                // keep six operand reads in flight ahead of the MFMAs
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, ahead, 0);
+#pragma unroll
+                for (int i = 0; i < n - ahead; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, ahead, 0);
             __builtin_amdgcn_sched_barrier(0);
             __builtin_amdgcn_s_setprio(0);
             __builtin_amdgcn_sched_barrier(0);
@@ -441,8 +473,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             end_phase(true);  // K(0) and V(0) have landed
             if (group == 0) {
                 auto step = [&](int j, auto stage) TA_INLINE {
-                    plan_copies(min(j + 1, nsteps - 1), 1 - (int)stage);
-                    do_m(stage, copy_hook);
+                    do_m(stage, copy_hook, std::false_type{}, [&]() TA_INLINE {
+                        plan_copies(min(j + 1, nsteps - 1), 1 - (int)stage);
+                    });
                     end_phase(false);
                     do_x(j);
                     end_phase(true);
@@ -456,13 +489,19 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
                     step(j, Stage0{});
                 end_phase(false);  // group 1's last vector phase
             } else {
+                // group 1's matrix phase of step j reads stage j & 1, which
+                // has landed before its vector phase of step j - 1: the
+                // phase's first fragments are read at the start of that phase
+                auto no_prep = []() {};
+                prefetch(0);
                 end_phase(false);  // group 0's first matrix phase
-                do_m(Stage0{}, no_hook);
+                do_m(Stage0{}, no_hook, std::true_type{}, no_prep);
                 end_phase(false);
                 auto step = [&](int j, auto stage) TA_INLINE {
+                    prefetch(stage);
                     do_x(j - 1);
                     end_phase(false);
-                    do_m(stage, no_hook);
+                    do_m(stage, no_hook, std::true_type{}, no_prep);
                     end_phase(false);
                 };
                 int j = 1;
