@@ -317,13 +317,14 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // malformed item: never touch memory outside it; poison the outputs.
     // Block-sparse schedules record the length of their k-tile lists.  List
     // items (kModeCausalList) read the k-tiles list[ka0 .. ka0 + ka1) of the
-    // tile-list section instead of two runs.
+    // tile-list section instead of two runs; only the list form of the kernel
+    // accepts them, and no form accepts another mode.
     const bool list_mode = LIST && mode == kModeCausalList;
     if (!header_ok(sched, a.total_tokens, a.n_items, kind) ||
         a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0) ||
         seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
         r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || kb0 < 0 || kb1 < kb0 ||
-        (!LIST && mode == kModeCausalList) ||
+        (mode != kModeStreaming && mode != kModeCausal && !list_mode) ||
         (list_mode ? (ka1 < 0 || kb1 != kb0 || (int64_t)ka0 + ka1 > a.list_words)
                    : ka1 < ka0) ||
         (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows)) {

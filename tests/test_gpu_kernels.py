@@ -176,8 +176,9 @@ def test_corrupt_device_schedule_poisons_outputs(kind):
     """A device schedule that does not match the launch is rejected by every
     workgroup, which fills its slice of O and LSE with NaN (together every
     element) instead of leaving stale values: the caller sees the failure.
-    Cases: a wrong magic word in the device header, and one malformed item
-    (rows past its sequence)."""
+    Cases: a wrong magic word in the device header, one malformed item
+    (rows past its sequence), and an item whose mode the launch does not
+    serve (a list item outside a block-sparse schedule, an unknown mode)."""
     cu = [0, 700, 1024]
     q, k, v = _cuda(*draw_qkv(cu, 8, 2, 128, 23))
     if kind == "blocksparse":
@@ -211,6 +212,17 @@ def test_corrupt_device_schedule_poisons_outputs(kind):
         torch.cuda.synchronize()
         assert bool(torch.isnan(o).any()), (kind, out_dtype, "item")
         plan.sched.copy_(good)
+        # an item mode the launch does not serve: a list item (mode 2) outside
+        # a block-sparse schedule, or an unknown mode
+        modes = (2, 7) if kind != "blocksparse" else (7,)
+        for mode in modes:
+            o.zero_()
+            lse.zero_()
+            plan.sched[item + 8] = mode  # I_MODE (word 8) of the last item
+            plan.run(q, k, v, o, lse, 0.1)
+            torch.cuda.synchronize()
+            assert bool(torch.isnan(o).any()), (kind, out_dtype, "mode", mode)
+            plan.sched.copy_(good)
         log(f"corrupt schedule {kind} {out_dtype}: outputs poisoned")
 
 
