@@ -84,6 +84,9 @@ struct FwdArgs {
     int32_t n_units;
     int32_t n_slots;
     int32_t upw;
+    // single-unit kernel: the first n_lead items (a Triangle schedule's Last
+    // split items) are interleaved with the others in launch order (0: none)
+    int32_t n_lead;
 };
 
 struct MergeArgs {
@@ -299,9 +302,20 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     const int g = bid % a.hkv;
     bid /= a.hkv;
     const int sub = bid % a.subtiles;
-    const int item = bid / a.subtiles;
+    int item = bid / a.subtiles;
     if (item >= a.n_items)
         return;
+    if (a.n_lead > 0) {
+        // Launch slot x runs lead item floor(x n_lead / n_items) when that
+        // count steps up at x, else the next of the other items: the lead
+        // items (Last splits, each a run of k-tiles along the sequence) are
+        // spread evenly through the launch, each beside the streaming q-tiles
+        // whose bands have just read its keys into L2, instead of all reading
+        // K and V from HBM at the start.  A bijection on [0, n_items).
+        const uint32_t x = (uint32_t)item, nl = (uint32_t)a.n_lead, ni = (uint32_t)a.n_items;
+        const uint32_t s0 = x * nl / ni, s1 = (x + 1) * nl / ni;
+        item = s1 > s0 ? (int)s0 : (int)(nl + x - s1);
+    }
     // The item words are read before the header is checked so that both
     // scalar loads are in flight together (the host has checked that the
     // schedule holds n_items items, so the read is in bounds either way).
@@ -2120,6 +2134,11 @@ FwdArgs make_args(const void *q, const void *k, const void *v, void *o,
     a.n_units = 0;
     a.n_slots = 0;
     a.upw = 1;
+    // Triangle schedules interleave their Last split items into the launch
+    // (the slot arithmetic is 32-bit unsigned: (n_items + 1) n_lead < 2^32)
+    const bool lead_fits = (uint64_t)(info->n_items + 1) * (uint64_t)info->n_last_items <
+                           ((uint64_t)1 << 32);
+    a.n_lead = info->kind == TA_KIND_TRIANGLE && lead_fits ? info->n_last_items : 0;
     return a;
 }
 
