@@ -2159,17 +2159,24 @@ hipError_t launch_units(int nw, dim3 grid, const FwdArgs &a, int kind, hipStream
 // for the single-unit kernel.  A unit boundary costs about as much as the
 // per-workgroup costs it removes (measured: about 10 K cycles, the
 // epilogue's normalisation, staging and stores beside the other group's
-// MFMAs), and the pass runs at a power-limited clock, so the multi-unit
-// kernel pays off only for short units (the paper's sink 8 / window 512
-// shape: 12 steps, 5 % faster; 36-step units at window 2048: 1-3 % slower).
-// For units of at most kShortUnitSteps steps: one workgroup per CU (256 CUs
-// over the kv heads) when its units' steps fit the LDS step table,
-// otherwise the fewest rounds of such workgroups whose units fit.  The
-// environment variable TRIATTN_UNITS_PER_WG, read at every launch,
-// overrides the count (1: the single-unit kernel) within the table limits:
-// for tests and tuning.
-constexpr int64_t kShortUnitSteps = 16;
-int units_per_wg(const FwdArgs &a, int kind, int nw, int64_t units, int32_t max_item_tiles)
+// MFMAs), the single-unit kernel reads K ahead where the multi-unit kernel
+// has no registers to, and the pass runs at a power-limited clock, so the
+// multi-unit kernel pays off only for short units, and less at d = 128 than
+// at d = 64: on the paper's sink 8 / window 512 shape (10-12 steps) it is
+// 4.6 % faster at d = 64 and about 1 % slower at d = 128 (four runs, each
+// within about 1 % noise); at d = 128 units of 4-8 steps come out even and
+// 36-step units at window 2048 6-10 % slower.  For units of at most
+// short_unit_steps(d) steps: one workgroup per CU (256 CUs over the kv
+// heads) when its units' steps fit the LDS step table, otherwise the fewest
+// rounds of such workgroups whose units fit.  The environment variable
+// TRIATTN_UNITS_PER_WG, read at every launch, overrides the count (1: the
+// single-unit kernel) within the table limits: for tests and tuning.
+int64_t short_unit_steps(int head_dim)
+{
+    return head_dim == 128 ? 8 : 16;
+}
+int units_per_wg(const FwdArgs &a, int kind, int nw, int64_t units, int32_t max_item_tiles,
+                 int head_dim)
 {
     if (kind != TA_KIND_TRIANGLE || nw < 5 || units > INT32_MAX ||
         a.total_tokens >= kMaxUnitsTokens || max_item_tiles < 1)
@@ -2181,7 +2188,7 @@ int units_per_wg(const FwdArgs &a, int kind, int nw, int64_t units, int32_t max_
         if (forced >= 1)
             return (int)std::max<int64_t>(1, std::min<int64_t>(forced, cap));
     }
-    if (cap < 2 || unit_steps > kShortUnitSteps)
+    if (cap < 2 || unit_steps > short_unit_steps(head_dim))
         return 1;
     const int64_t slots = std::max<int64_t>(1, 256 / a.hkv);
     for (int64_t rounds = 1;; ++rounds) {
@@ -2202,7 +2209,7 @@ ta_status launch_tiles(int kind, const FwdArgs &a_in, int32_t head_dim, int32_t 
     hipError_t err;
     // Triangle passes over workgroups of five to eight waves run several
     // units per workgroup (multi-unit kernel); the others one.
-    const int upw = units_per_wg(a, kind, nw, units, max_item_tiles);
+    const int upw = units_per_wg(a, kind, nw, units, max_item_tiles, head_dim);
     if (upw > 1) {
         a.n_units = (int32_t)units;
         a.upw = upw;
