@@ -106,14 +106,16 @@ struct MergeArgs {
     int32_t tile;  // rows of a merge item are at most one q-tile
 };
 
+// The tests combine with & (no short-circuit), so every header word is
+// loaded before any test: the loads go out together instead of one memory
+// round trip per test.
 __device__ __forceinline__ bool header_ok(const int32_t *s, int64_t total,
                                           int32_t n_items, int32_t kind)
 {
     const int64_t t = (int64_t)(uint32_t)s[H_TOTAL_LO] |
                       ((int64_t)s[H_TOTAL_HI] << 32);
-    return s[H_MAGIC] == TA_SCHEDULE_MAGIC &&
-           s[H_VERSION] == TA_SCHEDULE_VERSION && s[H_KIND] == kind &&
-           t == total && s[H_ITEMS] == n_items;
+    return (s[H_MAGIC] == TA_SCHEDULE_MAGIC) & (s[H_VERSION] == TA_SCHEDULE_VERSION) &
+           (s[H_KIND] == kind) & (t == total) & (s[H_ITEMS] == n_items);
 }
 
 // A schedule that does not match the launch (wrong header, malformed item)
@@ -334,14 +336,19 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // tile-list section instead of two runs; only the list form of the kernel
     // accepts them, and no form accepts another mode.
     const bool list_mode = LIST && mode == kModeCausalList;
-    if (!header_ok(sched, a.total_tokens, a.n_items, kind) ||
-        a.list_words != (kind == TA_KIND_BLOCKSPARSE ? sched[H_WINDOW] : 0) ||
-        seq_off < 0 || seq_len < 0 || seq_off + seq_len > a.total_tokens ||
-        r0 < 0 || r1 > seq_len || r0 >= r1 || ka0 < 0 || kb0 < 0 || kb1 < kb0 ||
-        (mode != kModeStreaming && mode != kModeCausal && !list_mode) ||
-        (list_mode ? (ka1 < 0 || kb1 != kb0 || (int64_t)ka0 + ka1 > a.list_words)
-                   : ka1 < ka0) ||
-        (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows)) {
+    // One combined test without short-circuits: the header and item words
+    // are all loaded before it.
+    const int32_t list_len = sched[H_WINDOW];  // block-sparse: length of the lists
+    const bool bad =
+        !header_ok(sched, a.total_tokens, a.n_items, kind) |
+        (a.list_words != (kind == TA_KIND_BLOCKSPARSE ? list_len : 0)) |
+        (seq_off < 0) | (seq_len < 0) | (seq_off + seq_len > a.total_tokens) | (r0 < 0) |
+        (r1 > seq_len) | (r0 >= r1) | (ka0 < 0) | (kb0 < 0) | (kb1 < kb0) |
+        (mode != kModeStreaming && mode != kModeCausal && !list_mode) |
+        (list_mode ? (ka1 < 0) | (kb1 != kb0) | ((int64_t)ka0 + ka1 > a.list_words)
+                   : ka1 < ka0) |
+        ((part_base >= 0) & (part_base + (r1 - r0) > a.n_partial_rows));
+    if (bad) {
         poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x,
                        gridDim.x);
         return;

@@ -81,13 +81,15 @@ __device__ __forceinline__ int probe_swz(int r)
     return D == 128 ? (r & 15) : ((r >> 1) & 7);
 }
 
+// The tests combine with & (no short-circuit), so every header word is
+// loaded before any test: one memory round trip instead of one per test.
 __device__ __forceinline__ bool probe_header_ok(const int32_t *s, int64_t total,
                                                 int32_t n_items, int32_t tile, int64_t kept)
 {
     const int64_t t = (int64_t)(uint32_t)s[H_TOTAL_LO] | ((int64_t)s[H_TOTAL_HI] << 32);
-    return s[H_MAGIC] == TA_SCHEDULE_MAGIC && s[H_VERSION] == TA_SCHEDULE_VERSION &&
-           s[H_KIND] == TA_KIND_CAUSAL && s[H_TILE] == tile && t == total &&
-           s[H_ITEMS] == n_items && s[H_KEPT_TILES] == kept;
+    return (s[H_MAGIC] == TA_SCHEDULE_MAGIC) & (s[H_VERSION] == TA_SCHEDULE_VERSION) &
+           (s[H_KIND] == TA_KIND_CAUSAL) & (s[H_TILE] == tile) & (t == total) &
+           (s[H_ITEMS] == n_items) & (s[H_KEPT_TILES] == kept);
 }
 
 template <int D, int NW>
@@ -265,10 +267,11 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
         const int32_t ka0 = it[I_KA0], ka1 = it[I_KA1];
         const int64_t cost = it[I_COST];
         // guard against a malformed schedule: never touch memory outside it
-        ok = it[I_MODE] == kModeCausal && it[I_KB0] == it[I_KB1] && seq_off >= 0 &&
-             seq_len > 0 && seq_off + seq_len <= a.total_tokens && r0 >= 0 && r0 < r1 &&
-             r1 <= seq_len && ka0 >= 0 && ka1 >= ka0 && cost == ka1 - ka0 &&
-             ka1 <= (seq_len + a.tile - 1) / a.tile;
+        // (& without short-circuits: the item words are loaded together)
+        ok = (it[I_MODE] == kModeCausal) & (it[I_KB0] == it[I_KB1]) & (seq_off >= 0) &
+             (seq_len > 0) & (seq_off + seq_len <= a.total_tokens) & (r0 >= 0) & (r0 < r1) &
+             (r1 <= seq_len) & (ka0 >= 0) & (ka1 >= ka0) & (cost == ka1 - ka0) &
+             ((int64_t)ka1 * a.tile < (int64_t)seq_len + a.tile);
         if (!ok)
             break;
         const int s0 = (int)max<int64_t>(lo - pre, 0);
