@@ -683,16 +683,33 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     };
 
     // Element mask (branch-free selects) where the step crosses the diagonal
-    // or the window edge; keys beyond the sequence are beyond every row.
+    // or the window edge; keys beyond the sequence are beyond every row.  The
+    // cases are told apart per wave, so that a step needs one compare per
+    // score where only one bound applies: the causal bound on the diagonal,
+    // the sink bound on a step before every row's window, the window bound
+    // at the window edge; both only where a step holds more than one edge.
     auto mask_step = [&](int key0, f32x16 (&sacc)[2]) TA_INLINE {
-        const int lim = my_row - key0 - 8 * half;        // key offset <= lim
-        // streaming rows also need offset < sink_lim or offset > win_lim
-        const bool stream_mode = mode == kModeStreaming;
-        const int sink_lim = stream_mode ? a.sink - key0 - 8 * half : kStep;
-        const int win_lim = stream_mode ? lim - a.window : -1;
-        if (stream_mode && key0 + kStep - 1 <= row_base - a.window) {
-            // a step before every row's window (and before its diagonal):
-            // only its sink keys are kept
+        const int lim = my_row - key0 - 8 * half;  // key offset <= lim: causal
+        const bool need_causal = key0 + kStep - 1 > row_base;
+        const bool need_window = mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
+                                 row_hi - key0 >= a.window;
+        if (!need_window) {
+            // every key is a sink key or inside every row's window
+            if (need_causal) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int off = kb * 32 + key_of_reg(v, 0);
+                        sacc[kb][v] = off <= lim ? sacc[kb][v] : -INFINITY;
+                    }
+            }
+            return;
+        }
+        const int win_lim = lim - a.window;             // offset > win_lim: in the window
+        const int sink_lim = a.sink - key0 - 8 * half;  // offset < sink_lim: a sink key
+        if (key0 + kStep - 1 <= row_base - a.window) {
+            // before every row's window (and diagonal): only sink keys remain
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -702,13 +719,32 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 }
             return;
         }
+        if (!need_causal && key0 >= a.sink) {
+            // past the sink and before every row's diagonal: the window edge
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int off = kb * 32 + key_of_reg(v, 0);
+                    sacc[kb][v] = off > win_lim ? sacc[kb][v] : -INFINITY;
+                }
+            return;
+        }
+        // several bounds: sign-bit masks (all ones where kept) in vector
+        // registers, combined and applied with bit operations.  The score is
+        // copied out of the vector before its bits are taken: a bit cast of
+        // a vector element itself compiles to a read of element 0.
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int off = kb * 32 + key_of_reg(v, 0);  // 8 half is in lim
-                const bool keep = (off <= lim) & ((off < sink_lim) | (off > win_lim));
-                sacc[kb][v] = keep ? sacc[kb][v] : -INFINITY;
+                const int m = ~((lim - off) >> 31) &
+                              (((off - sink_lim) >> 31) | ((win_lim - off) >> 31));
+                const float sc = sacc[kb][v];
+                sacc[kb][v] = __builtin_bit_cast(
+                    float, (__builtin_bit_cast(uint32_t, sc) & (uint32_t)m) |
+                               (0xff800000u & ~(uint32_t)m));
             }
     };
     auto step_needs_mask = [&](int key0) TA_INLINE -> bool {
@@ -719,6 +755,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
 
     float m_ref = -INFINITY;  // reference maximum of the row, log2 domain
     float l_run = 0.f;        // running sum over this lane's keys
+    bool fresh = true;        // the first softmax: no reference maximum on any lane
 
     // Online softmax of one step: probabilities relative to the (lazily
     // re-based) reference maximum, converted to the bf16 B operand of PV.
@@ -749,7 +786,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 }
             return psum;
         };
-        float psum = exp_step(m_ref == -INFINITY ? 0.f : m_ref);
+        // The first step has no reference on any lane: it goes straight to
+        // the re-base (its first pass would be discarded).
+        float psum = INFINITY;
+        if (!fresh)
+            psum = exp_step(m_ref == -INFINITY ? 0.f : m_ref);
+        fresh = false;
         const bool bad = !(psum <= kRescaleBound) || m_ref == -INFINITY;
         if (__builtin_amdgcn_ballot_w64(bad) != 0) {
             float mx = -INFINITY;
