@@ -688,11 +688,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // score where only one bound applies: the causal bound on the diagonal,
     // the sink bound on a step before every row's window, the window bound
     // at the window edge; both only where a step holds more than one edge.
-    auto mask_step = [&](int key0, f32x16 (&sacc)[2]) TA_INLINE {
+    auto mask_step = [&](int key0, bool need_causal, bool need_window,
+                         f32x16 (&sacc)[2]) TA_INLINE {
         const int lim = my_row - key0 - 8 * half;  // key offset <= lim: causal
-        const bool need_causal = key0 + kStep - 1 > row_base;
-        const bool need_window = mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
-                                 row_hi - key0 >= a.window;
         if (!need_window) {
             // every key is a sink key or inside every row's window
             if (need_causal) {
@@ -746,11 +744,6 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                     float, (__builtin_bit_cast(uint32_t, sc) & (uint32_t)m) |
                                (0xff800000u & ~(uint32_t)m));
             }
-    };
-    auto step_needs_mask = [&](int key0) TA_INLINE -> bool {
-        return (key0 + kStep - 1 > row_base) ||
-               (mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
-                row_hi - key0 >= a.window);
     };
 
     float m_ref = -INFINITY;  // reference maximum of the row, log2 domain
@@ -863,8 +856,12 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     };
     auto do_x = [&](int j) TA_INLINE {
         const int key0 = step_key0(j);
-        if (step_needs_mask(key0))
-            mask_step(key0, s_acc);
+        // the step crosses its rows' diagonal, or a window edge
+        const bool need_causal = key0 + kStep - 1 > row_base;
+        const bool need_window = mode == kModeStreaming && key0 + kStep - 1 >= a.sink &&
+                                 row_hi - key0 >= a.window;
+        if (__builtin_expect(need_causal | need_window, 0))  // a few steps per item
+            mask_step(key0, need_causal, need_window, s_acc);
         softmax(s_acc, p_acc);
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
