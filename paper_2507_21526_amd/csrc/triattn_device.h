@@ -52,6 +52,33 @@ __device__ __forceinline__ void copy_to_lds16(const void *gbase, uint32_t lane_b
                  : "v"(lane_byte_off), "s"(gbase), "{m0}"(lds_addr));
 }
 
+// A burst of N (2 or 4) such copies into consecutive 1 KB blocks of LDS
+// from lds_addr on, with one M0 write and one wait state for all of them:
+// copy i uses the instruction offset i KB, which the hardware adds to both
+// the global and the LDS address, so its lane offset is its byte offset in
+// global memory minus i KB (never negative for the tiles copied here).
+template <int N>
+__device__ __forceinline__ void copy_burst_to_lds16(const void *gbase, const uint32_t (&off)[N],
+                                                    uint32_t lds_addr)
+{
+    static_assert(N == 2 || N == 4, "bursts of two or four copies");
+    if constexpr (N == 4)
+        asm volatile("s_nop 0\n\t"
+                     "global_load_lds_dwordx4 %0, %4\n\t"
+                     "global_load_lds_dwordx4 %1, %4 offset:1024\n\t"
+                     "global_load_lds_dwordx4 %2, %4 offset:2048\n\t"
+                     "global_load_lds_dwordx4 %3, %4 offset:3072"
+                     :
+                     : "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(gbase),
+                       "{m0}"(lds_addr));
+    else
+        asm volatile("s_nop 0\n\t"
+                     "global_load_lds_dwordx4 %0, %2\n\t"
+                     "global_load_lds_dwordx4 %1, %2 offset:1024"
+                     :
+                     : "v"(off[0]), "v"(off[1]), "s"(gbase), "{m0}"(lds_addr));
+}
+
 // Workgroup barrier without a memory fence: this wave's LDS reads are
 // complete (lgkmcnt 0); copies into LDS are synchronised by vmcnt waits.
 __device__ __forceinline__ void barrier_no_fence()

@@ -543,6 +543,18 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         if constexpr (!COPIER)
             copy_hook(slot);
     };
+    // Burst form of group 0's copies, for workgroups whose K/V tiles all lie
+    // inside the sequence (nothing to clamp): copy wave w copies the
+    // consecutive 1 KB blocks w * COPIES .. w * COPIES + COPIES - 1 of a
+    // tile in one burst with one M0 write, K after the copy slot of the first
+    // K copy and V after that of the first V copy.  Its lane offsets are
+    // constants of the lane (row * pitch + swizzled chunk - i KB, i the
+    // block's index in the burst, which the instruction offset adds back).
+    constexpr bool BURST =
+        !COPIER && (COPIES == 2 || COPIES == 4) && N_DMA == COPIES * N_COPY_WAVES;
+    constexpr int BURST_K_SLOT = COPY_STRIDE - 1;
+    constexpr int BURST_V_SLOT = COPIES * COPY_STRIDE + COPY_STRIDE - 1;
+    const uint32_t burst_lds = (uint32_t)(copy_rank * (COPIES - 1) * 1024);
 
     // S^T = K Q^T for one 64-key step from LDS stage `buf`; the two 32-key
     // accumulator chains alternate so that dependent MFMAs do not stall.
@@ -930,42 +942,88 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         if constexpr (Q_IN_STAGE)
             end_phase(false);  // stage 1 is free once every wave has read its Q
         if (group == 0) {
-            // j = 0: QK only, then the copies of the PV slots.
-            auto prep0 = [&]() TA_INLINE {
-                if constexpr (!COPIER)
-                    plan_step_copies(0, Stage0{});
-            };
-            do_m(Stage0{}, true, false, g0_hook, std::false_type{}, prep0);
-            if constexpr (!COPIER) {
+            auto run_group0 = [&](auto burst) TA_INLINE {
+                constexpr bool B = decltype(burst)::value;
+                uint32_t bk[B ? COPIES : 1], bv[B ? COPIES : 1];
+                if constexpr (B) {
 #pragma unroll
-                for (int c = 0; c < 2 * COPIES; ++c)
-                    if (c * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
-                        issue_slot(c);
-            }
-            end_phase(false);
-            do_x(0);
-            end_phase(true);
-            // step j reads stage j & 1 (odd j first)
-            auto step = [&](int j, auto stage) TA_INLINE {
-                auto prep = [&]() TA_INLINE {
-                    if constexpr (!COPIER)
-                        plan_step_copies(j, stage);
+                    for (int i = 0; i < COPIES; ++i) {
+                        const int row = (copy_rank * COPIES + i) * ROWS_PER_DMA + dma_row_in;
+                        const uint32_t ro = __umul24((uint32_t)row, row_stride_bytes) -
+                                            (uint32_t)(i * 1024);
+                        bk[i] = ro + (uint32_t)((dma_pc ^ kswz<D>(row)) << 4);
+                        bv[i] = ro + (uint32_t)((dma_pc ^ vswz<D>(row)) << 4);
+                    }
+                }
+                auto burst_k = [&]() TA_INLINE {
+                    if constexpr (B)
+                        copy_burst_to_lds16<COPIES>(cp_k.base, bk, cp_k.lds + burst_lds);
                 };
-                do_m(stage, true, true, g0_hook, std::false_type{}, prep);
+                auto burst_v = [&]() TA_INLINE {
+                    if constexpr (B)
+                        copy_burst_to_lds16<COPIES>(cp_v.base, bv, cp_v.lds + burst_lds);
+                };
+                auto hook = [&](int slot) TA_INLINE {
+                    if constexpr (B) {
+                        if (slot == BURST_K_SLOT)
+                            burst_k();
+                        else if (slot == BURST_V_SLOT)
+                            burst_v();
+                    } else {
+                        g0_hook(slot);
+                    }
+                };
+                // j = 0: QK only, then the copies of the PV slots.
+                auto prep0 = [&]() TA_INLINE {
+                    if constexpr (!COPIER)
+                        plan_step_copies(0, Stage0{});
+                };
+                do_m(Stage0{}, true, false, hook, std::false_type{}, prep0);
+                if constexpr (B) {
+                    if constexpr (BURST_V_SLOT >= 2 * QK_STEPS)
+                        burst_v();
+                } else if constexpr (!COPIER) {
+#pragma unroll
+                    for (int c = 0; c < 2 * COPIES; ++c)
+                        if (c * COPY_STRIDE + COPY_STRIDE - 1 >= 2 * QK_STEPS)
+                            issue_slot(c);
+                }
                 end_phase(false);
-                do_x(j);
+                do_x(0);
                 end_phase(true);
+                // step j reads stage j & 1 (odd j first)
+                auto step = [&](int j, auto stage) TA_INLINE {
+                    auto prep = [&]() TA_INLINE {
+                        if constexpr (!COPIER)
+                            plan_step_copies(j, stage);
+                    };
+                    do_m(stage, true, true, hook, std::false_type{}, prep);
+                    end_phase(false);
+                    do_x(j);
+                    end_phase(true);
+                };
+                int j = 1;
+                for (; j + 1 < nsteps; j += 2) {
+                    step(j, Stage1{});
+                    step(j + 1, Stage0{});
+                }
+                if (j < nsteps)
+                    step(j, Stage1{});
+                do_m(nsteps & 1, false, true, no_hook, std::false_type{}, no_prep);
+                end_phase(false);
+                end_phase(false);
             };
-            int j = 1;
-            for (; j + 1 < nsteps; j += 2) {
-                step(j, Stage1{});
-                step(j + 1, Stage0{});
+            // The steps' keys increase, so every tile lies inside the
+            // sequence when the last step's does (the copies past the last
+            // step repeat it).
+            if constexpr (BURST) {
+                if (step_key0(nsteps - 1) + kStep - 1 <= key_max)
+                    run_group0(std::true_type{});
+                else
+                    run_group0(std::false_type{});
+            } else {
+                run_group0(std::false_type{});
             }
-            if (j < nsteps)
-                step(j, Stage1{});
-            do_m(nsteps & 1, false, true, no_hook, std::false_type{}, no_prep);
-            end_phase(false);
-            end_phase(false);
         } else {
             // Group 1's matrix phase M(j) reads stage j & 1, whose K(j) has
             // landed before the phase in which group 1 runs X(j - 1): the
