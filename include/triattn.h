@@ -43,8 +43,13 @@
  *   returns a nonzero ta_status, launches nothing, leaves every output
  *   untouched and records a message that ta_last_error() returns (per
  *   thread).  No C++ exception crosses this interface.  The kernels also
- *   check the schedule header against the launch arguments and write nothing
- *   if it does not match.
+ *   check the device schedule against the launch arguments: a header that
+ *   does not match makes every workgroup fill its share of O (and LSE) with
+ *   NaN, so that every element is NaN; an item whose words are out of range
+ *   or whose mode the launch does not serve is not computed, and its
+ *   workgroups fill the rows it names (clamped into the buffers, one q-tile
+ *   at most) with NaN, so that the failure is visible in the output.  No
+ *   access leaves the caller's buffers either way.
  */
 #ifndef TRIATTN_H
 #define TRIATTN_H

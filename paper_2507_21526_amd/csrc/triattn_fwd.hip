@@ -144,6 +144,44 @@ __device__ __forceinline__ void poison_outputs(void *o, int o_f32, float *lse,
         lse[i] = __builtin_nanf("");
 }
 
+// A rejected item's own rows (every head), as far as its words say where
+// they are (clamped into the buffers, one q-tile at most), filled with NaN,
+// and its split partial rows when it names some: no other workgroup writes
+// these rows (a split item's O rows are the merge's, which then reads the
+// NaN partials), so a malformed item is visible in O and LSE, which the
+// slice of poison_outputs alone does not ensure (later workgroups may
+// overwrite that slice).  Every index stays inside the buffers the host
+// checked, whatever the words hold.
+__device__ __forceinline__ void poison_item_rows(void *o, int o_f32, float *lse, float *part_o,
+                                                 float *part_lse, int64_t total_tokens,
+                                                 int32_t hq, int d, int64_t n_partial_rows,
+                                                 int tile, int64_t seq_off, int64_t r0,
+                                                 int64_t r1, int64_t part_base)
+{
+    const int64_t lo = min(max(seq_off + r0, (int64_t)0), total_tokens);
+    int64_t hi = min(max(seq_off + r1, lo), lo + tile);
+    if (hi == lo)
+        hi = lo + tile;  // an empty or reversed row range: the tile from lo
+    hi = min(hi, total_tokens);
+    const int64_t rows = hi - lo;
+    for (int64_t i = threadIdx.x; i < rows * hq * d; i += blockDim.x) {
+        if (o_f32)
+            reinterpret_cast<float *>(o)[lo * hq * d + i] = __builtin_nanf("");
+        else
+            reinterpret_cast<uint16_t *>(o)[lo * hq * d + i] = 0x7fc0;  // bf16 quiet NaN
+    }
+    if (lse)
+        for (int64_t i = threadIdx.x; i < rows * hq; i += blockDim.x)
+            lse[(i / rows) * total_tokens + lo + i % rows] = __builtin_nanf("");
+    if (part_o && part_base >= 0 && part_base < n_partial_rows) {
+        const int64_t prows = min(rows, n_partial_rows - part_base);
+        for (int64_t i = threadIdx.x; i < prows * hq * d; i += blockDim.x)
+            part_o[part_base * hq * d + i] = __builtin_nanf("");
+        for (int64_t i = threadIdx.x; i < prows * hq; i += blockDim.x)
+            part_lse[part_base * hq + i] = __builtin_nanf("");
+    }
+}
+
 // Key offset (within a 32-key block) held by register v of lane half h in
 // the S^T accumulator, given the permuted K row order.
 __device__ __forceinline__ int key_of_reg(int v, int h)
@@ -351,6 +389,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     if (bad) {
         poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x,
                        gridDim.x);
+        poison_item_rows(a.o, a.o_f32, a.lse, a.part_o, a.part_lse, a.total_tokens, a.hq, D,
+                         a.n_partial_rows, a.tile, seq_off, r0, r1, part_base);
         return;
     }
     const int32_t *tile_list = sched + a.list_base + (list_mode ? ka0 : 0);
@@ -915,13 +955,46 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 end_phase(true);
                 if constexpr (Q_IN_STAGE)
                     end_phase(false);
-                for (int j = 0; j < nsteps; ++j) {
-                    plan_step_copies(j, j & 1);
+                // When every tile lies inside the sequence (the steps' keys
+                // increase, so when the last one does), the copies go out in
+                // bursts of four consecutive 1 KB blocks: one M0 write per
+                // burst, the blocks placed by the instruction offset, and the
+                // burst's rows reached through the scalar base, so that four
+                // lane offsets per tensor serve every burst.
+                if (step_key0(nsteps - 1) + kStep - 1 <= key_max) {
+                    constexpr int GROUP_ROWS = 4 * ROWS_PER_DMA;
+                    static_assert(N_DMA % 4 == 0, "whole bursts of four copies");
+                    uint32_t bk[4], bv[4];
 #pragma unroll
-                    for (int c = 0; c < 2 * COPIES; ++c)
-                        issue_slot(c);
-                    end_phase(false);
-                    end_phase(true);
+                    for (int i = 0; i < 4; ++i) {
+                        const int row = i * ROWS_PER_DMA + dma_row_in;
+                        const uint32_t ro = __umul24((uint32_t)row, row_stride_bytes) -
+                                            (uint32_t)(i * 1024);
+                        bk[i] = ro + (uint32_t)((dma_pc ^ kswz<D>(row)) << 4);
+                        bv[i] = ro + (uint32_t)((dma_pc ^ vswz<D>(row)) << 4);
+                    }
+                    for (int j = 0; j < nsteps; ++j) {
+                        plan_step_copies(j, j & 1);
+#pragma unroll
+                        for (int g4 = 0; g4 < N_DMA / 4; ++g4)
+                            copy_burst_to_lds16<4>(cp_k.base + g4 * GROUP_ROWS * tok_stride, bk,
+                                                   cp_k.lds + g4 * 4096);
+#pragma unroll
+                        for (int g4 = 0; g4 < N_DMA / 4; ++g4)
+                            copy_burst_to_lds16<4>(cp_v.base + g4 * GROUP_ROWS * tok_stride, bv,
+                                                   cp_v.lds + g4 * 4096);
+                        end_phase(false);
+                        end_phase(true);
+                    }
+                } else {
+                    for (int j = 0; j < nsteps; ++j) {
+                        plan_step_copies(j, j & 1);
+#pragma unroll
+                        for (int c = 0; c < 2 * COPIES; ++c)
+                            issue_slot(c);
+                        end_phase(false);
+                        end_phase(true);
+                    }
                 }
                 end_phase(false);
                 end_phase(false);
@@ -1452,6 +1525,8 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
             (part_base >= 0 && part_base + (r1 - r0) > a.n_partial_rows)) {
             poison_outputs(a.o, a.o_f32, a.lse, a.total_tokens, a.hq, D, blockIdx.x,
                            gridDim.x);
+            poison_item_rows(a.o, a.o_f32, a.lse, a.part_o, a.part_lse, a.total_tokens, a.hq,
+                             D, a.n_partial_rows, a.tile, seq_off, r0, r1, part_base);
             return;
         }
         const int sub = (slot + k * a.n_slots) % a.subtiles;

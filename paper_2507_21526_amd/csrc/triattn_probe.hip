@@ -248,6 +248,34 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             issue_slot(slot_ / COPY_STRIDE);
     };
     auto no_hook = [](int) {};
+    // Burst form of the copies, for chunks whose K/V tiles all lie inside
+    // the sequence (nothing to clamp): copy wave w copies the consecutive
+    // 1 KB blocks w * COPIES .. w * COPIES + COPIES - 1 of a tile in one burst
+    // with one M0 write, at the copy slots of the first K and the first V
+    // copy; its lane offsets (row * pitch + swizzled chunk - i KB, i the
+    // block's index in the burst, which the instruction offset adds back)
+    // are constants of the lane.
+    constexpr bool BURST = (COPIES == 2 || COPIES == 4) && N_DMA == COPIES * N_COPY_WAVES;
+    constexpr int BURST_K_SLOT = COPY_STRIDE - 1;
+    constexpr int BURST_V_SLOT = COPIES * COPY_STRIDE + COPY_STRIDE - 1;
+    uint32_t boff[BURST ? COPIES : 1];
+    if constexpr (BURST) {
+#pragma unroll
+        for (int i = 0; i < COPIES; ++i) {
+            const int row = (wave * COPIES + i) * ROWS_PER_DMA + dma_row_in;
+            boff[i] = __umul24((uint32_t)row, row_stride_bytes) - (uint32_t)(i * 1024) +
+                      (uint32_t)((dma_pc ^ probe_swz<D>(row)) << 4);
+        }
+    }
+    auto burst_hook = [&](int slot_) TA_INLINE {
+        if constexpr (BURST) {
+            const uint32_t blk = cp.lds + (uint32_t)(wave * COPIES * 1024);
+            if (slot_ == BURST_K_SLOT)
+                copy_burst_to_lds16<COPIES>(cp.kb, boff, blk);
+            else if (slot_ == BURST_V_SLOT)
+                copy_burst_to_lds16<COPIES>(cp.vb, boff, blk + TILE_BYTES);
+        }
+    };
     auto end_phase = [&](bool wait_copies) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
         if (wait_copies)
@@ -475,21 +503,39 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             }
             end_phase(true);  // K(0) and V(0) have landed
             if (group == 0) {
-                auto step = [&](int j, auto stage) TA_INLINE {
-                    do_m(stage, copy_hook, std::false_type{}, [&]() TA_INLINE {
-                        plan_copies(min(j + 1, nsteps - 1), 1 - (int)stage);
-                    });
-                    end_phase(false);
-                    do_x(j);
-                    end_phase(true);
+                auto run_group0 = [&](auto burst) TA_INLINE {
+                    auto hook = [&](int slot_) TA_INLINE {
+                        if constexpr (decltype(burst)::value)
+                            burst_hook(slot_);
+                        else
+                            copy_hook(slot_);
+                    };
+                    auto step = [&](int j, auto stage) TA_INLINE {
+                        do_m(stage, hook, std::false_type{}, [&]() TA_INLINE {
+                            plan_copies(min(j + 1, nsteps - 1), 1 - (int)stage);
+                        });
+                        end_phase(false);
+                        do_x(j);
+                        end_phase(true);
+                    };
+                    int j = 0;
+                    for (; j + 1 < nsteps; j += 2) {
+                        step(j, Stage0{});
+                        step(j + 1, Stage1{});
+                    }
+                    if (j < nsteps)
+                        step(j, Stage0{});
                 };
-                int j = 0;
-                for (; j + 1 < nsteps; j += 2) {
-                    step(j, Stage0{});
-                    step(j + 1, Stage1{});
+                // the chunk's steps are contiguous: every tile lies inside
+                // the sequence when the last one does
+                if constexpr (BURST) {
+                    if (key_begin + nsteps * kProbeStep - 1 <= key_max)
+                        run_group0(std::true_type{});
+                    else
+                        run_group0(std::false_type{});
+                } else {
+                    run_group0(std::false_type{});
                 }
-                if (j < nsteps)
-                    step(j, Stage0{});
                 end_phase(false);  // group 1's last vector phase
             } else {
                 // group 1's matrix phase of step j reads stage j & 1, which

@@ -173,12 +173,15 @@ def test_split_invariance():
 
 @pytest.mark.parametrize("kind", ["triangle", "causal", "blocksparse"])
 def test_corrupt_device_schedule_poisons_outputs(kind):
-    """A device schedule that does not match the launch is rejected by every
-    workgroup, which fills its slice of O and LSE with NaN (together every
-    element) instead of leaving stale values: the caller sees the failure.
-    Cases: a wrong magic word in the device header, one malformed item
-    (rows past its sequence), and an item whose mode the launch does not
-    serve (a list item outside a block-sparse schedule, an unknown mode)."""
+    """A device schedule that does not match the launch is rejected: with a
+    bad header every workgroup fills its slice of O and LSE with NaN
+    (together every element); a rejected item's workgroups fill the rows it
+    names, which no other workgroup writes, so the NaN is there whatever
+    order the workgroups run in.  Either way the caller sees the failure
+    instead of stale values.  Cases: a wrong magic word in the device
+    header, one malformed item (rows past its sequence), and an item whose
+    mode the launch does not serve (a list item outside a block-sparse
+    schedule, an unknown mode)."""
     cu = [0, 700, 1024]
     q, k, v = _cuda(*draw_qkv(cu, 8, 2, 128, 23))
     if kind == "blocksparse":
