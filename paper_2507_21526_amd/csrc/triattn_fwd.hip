@@ -799,6 +799,10 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     };
 
     float m_ref = -INFINITY;  // reference maximum of the row, log2 domain
+    // the maximum the probabilities are taken against: m_ref once set; while
+    // it is -inf, a plain pass yields an infinite or NaN sum, which sends the
+    // step to the re-base as an unset maximum must
+    float m_cur = -INFINITY;
     float l_run = 0.f;        // running sum over this lane's keys
     bool fresh = true;        // the first softmax: no reference maximum on any lane
 
@@ -825,7 +829,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                     for (int e = 0; e < 8; ++e) {
                         t[e] = __builtin_amdgcn_exp2f(
                             __builtin_fmaf(sacc[kb][8 * s2 + e], c, -m_use));
-                        psum += t[e];
+                        // the sum starts at the first term (exp2 is never -0)
+                        psum = (kb | s2 | e) ? psum + t[e] : t[e];
                     }
                     pf[kb][s2] = __builtin_convertvector(t, bf16x8);
                 }
@@ -835,9 +840,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         // the re-base (its first pass would be discarded).
         float psum = INFINITY;
         if (!fresh)
-            psum = exp_step(m_ref == -INFINITY ? 0.f : m_ref);
+            psum = exp_step(m_cur);
         fresh = false;
-        const bool bad = !(psum <= kRescaleBound) || m_ref == -INFINITY;
+        const bool bad = !(psum <= kRescaleBound);
         if (__builtin_amdgcn_ballot_w64(bad) != 0) {
             float mx = -INFINITY;
 #pragma unroll
@@ -854,6 +859,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
             for (int b = 0; b < D_BLOCKS; ++b)
                 oacc[b] *= alpha;
             m_ref = m_new;
+            m_cur = m_new;
             psum = exp_step(m_use);
         }
         l_run += psum;
@@ -922,6 +928,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 fence_regs(p_acc[kb][s2]);
         fence_regs(l_run);
         fence_regs(m_ref);
+        fence_regs(m_cur);
     };
     // A phase boundary: the scheduler may not move any instruction across it
     // (MFMAs and VALU work must stay in their own phase).
@@ -1822,6 +1829,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
     };
 
     float m_ref = -INFINITY;
+    float m_cur = -INFINITY;  // as in the single-unit kernel
     float l_run = 0.f;
     bool fresh = true;  // the unit's first softmax: no reference maximum on any lane
     auto softmax = [&](f32x16 (&sacc)[2], bf16x8 (&pf)[2][2]) TA_INLINE {
@@ -1836,7 +1844,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
                     for (int e = 0; e < 8; ++e) {
                         t[e] = __builtin_amdgcn_exp2f(
                             __builtin_fmaf(sacc[kb][8 * s2 + e], c, -m_use));
-                        psum += t[e];
+                        psum = (kb | s2 | e) ? psum + t[e] : t[e];  // exp2 is never -0
                     }
                     pf[kb][s2] = __builtin_convertvector(t, bf16x8);
                 }
@@ -1846,9 +1854,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         // straight to the re-base (its first pass would be discarded).
         float psum = INFINITY;
         if (!fresh)
-            psum = exp_step(m_ref == -INFINITY ? 0.f : m_ref);
+            psum = exp_step(m_cur);
         fresh = false;
-        const bool bad = !(psum <= kRescaleBound) || m_ref == -INFINITY;
+        const bool bad = !(psum <= kRescaleBound);
         if (__builtin_amdgcn_ballot_w64(bad) != 0) {
             float mx = -INFINITY;
 #pragma unroll
@@ -1865,6 +1873,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
             for (int b = 0; b < D_BLOCKS; ++b)
                 oacc[b] *= alpha;
             m_ref = m_new;
+            m_cur = m_new;
             psum = exp_step(m_use);
         }
         l_run += psum;
@@ -1921,6 +1930,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
                 fence_regs(p_acc[kb][s2]);
         fence_regs(l_run);
         fence_regs(m_ref);
+        fence_regs(m_cur);
     };
     auto end_phase = [&](bool wait_copies) TA_INLINE {
         __builtin_amdgcn_sched_barrier(0);
@@ -1939,6 +1949,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_units_kernel(FwdArgs a, int32
         for (int b = 0; b < D_BLOCKS; ++b)
             oacc[b] = f32x16{};
         m_ref = -INFINITY;
+        m_cur = -INFINITY;
         l_run = 0.f;
         fresh = true;
         rec_cur = rec_nxt;
