@@ -529,7 +529,9 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
     // byte offsets, which are monotonic in r), an unsigned 32-bit offset of
     // fewer than 64 rows that is never negative.  Everything that depends
     // only on the tile is computed once here, so a copy costs one M0 write,
-    // a nop, three vector instructions and the copy itself.
+    // a nop, the clamp and the copy itself.  Workgroups whose tiles all lie
+    // inside the sequence use the burst form instead (BURST below: no clamp,
+    // one M0 write per four copies).
     struct TileCopy {
         const uint16_t *base;  // row kc of the source
         uint32_t lds;          // LDS address of this wave's first copy
