@@ -121,8 +121,9 @@ const char *ta_last_error(void);
  *               causal).  last = 0 gives the Streaming pattern.
  *   tile        64 or 128.
  *   splits      0 = automatic: a Last q-tile with nk kept k-tiles gets
- *               ceil(nk / t) splits (at most nk), t = ceil(sink/tile) +
- *               ceil(window/tile) + 1; > 0 = that many (at most nk).
+ *               ceil(nk / t) splits (at most nk), t = max(ceil(sink/tile) +
+ *               ceil(window/tile) + 1, ceil(2048/tile)); > 0 = that many
+ *               (at most nk).
  *   out         host buffer of out_words int32, or NULL to query the size
  *               (info is filled either way).
  * Returns TA_OK, TA_ERR_INVALID_ARG, TA_ERR_UNSUPPORTED or

@@ -414,9 +414,11 @@ int64_t oracle_schedule(int kind, const int32_t *cu_seqlens, int32_t batch,
     item_vec last_items = {0}, main_items = {0}, merges = {0};
     int64_t partial_rows = 0, kept_total = 0, merged_rows = 0;
     int fail = 0;
-    /* steady-state streaming work of one q-tile, in k-tiles */
-    const int64_t t_star = (sink + tile - 1) / tile +
-                           (window + tile - 1) / tile + 1;
+    /* steady-state streaming work of one q-tile, in k-tiles, and at least
+     * 2048 keys' worth (reading 8: Algorithm 1 leaves the split count open) */
+    int64_t t_star = (sink + tile - 1) / tile + (window + tile - 1) / tile + 1;
+    if (t_star < (2048 + tile - 1) / tile)
+        t_star = (2048 + tile - 1) / tile;
 
     for (int32_t b = 0; b < batch && !fail; ++b) {
         const int64_t off = cu_seqlens[b];

@@ -132,8 +132,12 @@ extern "C" ta_status ta_build_schedule(int32_t kind, const int32_t *cu_seqlens,
 
     const int64_t T = tile;
     // Steady-state streaming work of one q-tile in k-tiles; the automatic
-    // rule sizes Last splits to about that much work each.
-    const int64_t t_star = ceil_div(sink, T) + ceil_div(window, T) + 1;
+    // rule sizes Last splits to about that much work each, but to no fewer
+    // than 2048 keys (32 steps of 64 keys), so that a split's fixed costs
+    // (workgroup set-up, its partial rows and their merge) stay small
+    // against its steps when the window is short.
+    const int64_t t_star =
+        std::max(ceil_div(sink, T) + ceil_div(window, T) + 1, ceil_div(2048, T));
 
     std::vector<Item> last_items, items;
     std::vector<Merge> merges;

@@ -73,13 +73,15 @@ def test_units_against_oracle():
 
 def test_units_noalloc_and_graph_replay():
     """The no-allocation entry point and HIP graph replays run the same
-    multi-unit launches: the library's own unit rule at the paper's sink 8 /
-    window 512 shape (12-step units) picks the multi-unit kernel."""
+    multi-unit launches: the library's own unit rule picks the multi-unit
+    kernel for this shape (sink 8, window 128 and 32 explicit Last splits:
+    items of at most 4 k-tiles, 8 steps at d = 128), which the single-unit
+    kernel (one unit per workgroup forced) must match bit for bit."""
     from paper_2507_21526_amd import binding
     cu, hq, hkv, d = [0, 16384], 32, 8, 128
     q, k, v = (t.cuda() for t in draw_qkv(cu, hq, hkv, d, seed=78))
-    plan = binding.Plan("triangle", cu, 8, 512, 128, 128, hq, d)
-    assert plan.info.max_item_tiles * 2 <= 16
+    plan = binding.Plan("triangle", cu, 8, 128, 128, 128, hq, d, splits=32)
+    assert plan.info.max_item_tiles * 2 <= 8
     ref = torch.empty(q.shape, dtype=torch.bfloat16, device=q.device)
     plan.run(q, k, v, ref, None, d ** -0.5)
     os.environ[ENV] = "1"
