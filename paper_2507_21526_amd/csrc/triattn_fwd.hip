@@ -596,6 +596,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
         !COPIER && (COPIES == 2 || COPIES == 4) && N_DMA == COPIES * N_COPY_WAVES;
     constexpr int BURST_K_SLOT = COPY_STRIDE - 1;
     constexpr int BURST_V_SLOT = COPIES * COPY_STRIDE + COPY_STRIDE - 1;
+    // from a planned copy's LDS address (block copy_rank of the tile) to the
+    // first block of this wave's burst (block copy_rank * COPIES)
     const uint32_t burst_lds = (uint32_t)(copy_rank * (COPIES - 1) * 1024);
 
     // S^T = K Q^T for one 64-key step from LDS stage `buf`; the two 32-key
@@ -1030,6 +1032,8 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void attn_tile_kernel(Fwd
                 if constexpr (B) {
 #pragma unroll
                     for (int i = 0; i < COPIES; ++i) {
+                        // row >= i * ROWS_PER_DMA rows of at least 1024 / ROWS_PER_DMA
+                        // bytes each, so subtracting i KB cannot wrap
                         const int row = (copy_rank * COPIES + i) * ROWS_PER_DMA + dma_row_in;
                         const uint32_t ro = __umul24((uint32_t)row, row_stride_bytes) -
                                             (uint32_t)(i * 1024);
