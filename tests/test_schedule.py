@@ -87,6 +87,28 @@ def test_schedule_workload_counts():
     assert info.n_partial_rows == 57 * 128 and info.n_last_rows == 128
 
 
+def test_automatic_split_counts():
+    """Reading of the split count (Algorithm 1 leaves it open): a Last q-tile
+    with nk kept k-tiles gets ceil(nk / t) splits, t = max(ceil(S/T) +
+    ceil(W/T) + 1, ceil(2048/T)); the values below are that arithmetic done
+    by hand for the 128K Last q-tile (nk = 1024 at T = 128, 2048 at T = 64)."""
+    cases = [
+        # S, W, T, expected splits
+        (128, 2048, 128, 57),   # t = 1 + 16 + 1 = 18: ceil(1024 / 18)
+        (128, 4096, 128, 31),   # t = 1 + 32 + 1 = 34: ceil(1024 / 34)
+        (8, 512, 128, 64),      # t = max(1 + 4 + 1, 16) = 16
+        (64, 128, 128, 64),     # t = max(1 + 1 + 1, 16) = 16
+        (8, 512, 64, 64),       # t = max(1 + 8 + 1, 32) = 32: ceil(2048 / 32)
+    ]
+    for S, W, T, want in cases:
+        _, info = binding.ta_build_schedule("triangle", [0, 131072], S, W, 128, T)
+        assert info.max_splits == want, (S, W, T, info.max_splits)
+    # a short sequence: the Last q-tile of 1024 tokens has 8 k-tiles, fewer
+    # than t = 16, so it is not split (one partial item and its merge)
+    _, info = binding.ta_build_schedule("triangle", [0, 1024], 8, 512, 128, 128)
+    assert info.max_splits == 1 and info.n_last_items == 1
+
+
 def test_schedule_llama_128k_matches_oracle():
     w = WORKLOADS["llama8b_n128k"]
     got, _, want = _both("triangle", w.cu_seqlens, w.sink, w.window, w.last,
