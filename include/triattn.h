@@ -316,9 +316,10 @@ ta_status blocksparse_attn_fwd(const void *q, const void *k, const void *v,
  *                0); its contents on entry do not matter.
  * Grad(M-hat_r, l) = sum_h region_sums[h * 3 + r] / (hq * count_r) with the
  * pair counts of ta_region_counts (ta_region_grad_mean).  The work is cut
- * into equal shares of kept k-tiles, one per workgroup, so the pass does not
- * wait on the longest q-tile.  The result is deterministic (fixed shares and
- * reduction order for a given shape).  Device schedule words that do not
+ * into equal shares of kept 64-key steps (plus a charge per q-tile change),
+ * one per workgroup, so the pass does not wait on the longest q-tile.  The
+ * result is deterministic (fixed shares and reduction order for a given
+ * shape).  Device schedule words that do not
  * match info give NaN sums.  Errors as triangle_attn_fwd.
  */
 size_t ta_probe_workspace_bytes(const ta_schedule_info *info, int32_t hq);

@@ -51,6 +51,11 @@ constexpr int kProbeStep = 64;  // keys per step
 constexpr float kProbeLog2e = 1.4426950408889634f;
 constexpr int kProbeCUs = 256;       // compute units of the MI355X
 constexpr int kProbeMaxSlots = 512;  // workgroups per (kv head, row block), at most
+// Cost of moving to the next item within a share, in 64-key steps: the
+// pipeline drains, and the new q-tile's Q, dO and LSE rows arrive before
+// its first matrix phase.  At 2K tokens charges of 3, 4 and 5 steps time the
+// same and 2 is 12 % slower; 4 is the middle of that range.
+constexpr int kProbeItemChange = 4;
 
 struct ProbeArgs {
     const uint16_t *q;
@@ -110,7 +115,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
     constexpr int NT = NW * 64;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE_BYTES];
     __shared__ int64_t wave_tot[NW];
-    __shared__ int64_t first[2];  // first item of the share, its cost prefix
+    __shared__ int64_t first[4];  // first item of the share, lo, its prefix, hi
 
     const int per_slot = a.subtiles * a.hkv;
     const int slot = blockIdx.x / per_slot;
@@ -135,34 +140,50 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
     // both loads are in flight together (the host has checked that the
     // schedule holds n_items items, so the reads are in bounds either way).
     bool ok = probe_header_ok(sched, a.total_tokens, a.n_items, a.tile, a.total_cost);
-    // The workgroup's share of kept k-tiles [lo, hi), counted over the items
-    // laid end to end in schedule order from `pre` at item `item`: one whole
-    // item (per-item launch), or an equal share of the total.
+    // The workgroup's share [lo, hi) of the kept 64-key steps (tile / 64 per
+    // kept k-tile), counted over the items laid end to end in schedule order
+    // from `pre` at item `item`: one whole item (per-item launch), or one of
+    // n_slots shares of the total.  The shares are equal in a virtual cost
+    // that charges each item kProbeItemChange steps on top of its own, placed
+    // before its first step, so a share that walks many short items gets
+    // fewer steps; a virtual position v inside item i (virtual prefix P) is
+    // the real position P - i * kProbeItemChange + max(0, v - P -
+    // kProbeItemChange).  At 2K tokens (16 items of 32, 30, .., 2 steps over
+    // 16 slots) equal k-tile shares give one share 18 steps over three
+    // items (four with equal step shares); virtual shares give the shares
+    // that walk many short items fewer steps.
+    const int spt = a.tile / kProbeStep;
+    const int64_t total_steps = (int64_t)spt * a.total_cost;
     int item = 0;
     int64_t pre = 0, lo = 0, hi = 0;
     if (a.per_item) {
         item = slot;
-        hi = sched[kHdrWords + (int64_t)item * kItemWords + I_COST];
+        hi = (int64_t)spt * sched[kHdrWords + (int64_t)item * kItemWords + I_COST];
     } else {
-        const int64_t per = (a.total_cost + a.n_slots - 1) / a.n_slots;
-        lo = min((int64_t)slot * per, a.total_cost);
-        hi = min(lo + per, a.total_cost);
-        pre = lo;  // an empty share is covered as it stands
-        if (lo < hi) {
-            // Item holding k-tile lo: thread t sums the costs of items
+        const int64_t vtotal = total_steps + (int64_t)kProbeItemChange * a.n_items;
+        const int64_t per = (vtotal + a.n_slots - 1) / a.n_slots;
+        const int64_t vlo = min((int64_t)slot * per, vtotal);
+        const int64_t vhi = min(vlo + per, vtotal);
+        lo = hi = pre = total_steps;  // an empty share is covered as it stands
+        item = a.n_items;
+        if (vlo < vhi) {
+            // Items holding virtual positions vlo and vhi: thread t sums the
+            // (virtual) costs of items
             // [t m, t m + m), a scan over the threads gives each its prefix,
-            // and the thread whose items contain lo records it.  The costs
-            // must add up to the header's total, none negative.
+            // and the threads whose items contain vlo and vhi record the
+            // share's bounds.  The costs must add up to the header's total,
+            // none negative.
             const int m = (a.n_items + NT - 1) / NT;
             const int i0 = min(tid * m, a.n_items), i1 = min(i0 + m, a.n_items);
-            auto cost_of = [&](int i) -> int64_t {
-                return sched[kHdrWords + (int64_t)i * kItemWords + I_COST];
+            auto cost_of = [&](int i) -> int64_t {  // virtual, in steps
+                return (int64_t)spt * sched[kHdrWords + (int64_t)i * kItemWords + I_COST] +
+                       kProbeItemChange;
             };
             int64_t tsum = 0;
             bool neg = false;
             for (int i = i0; i < i1; ++i) {
                 const int64_t c = cost_of(i);
-                neg |= c < 0;
+                neg |= c < kProbeItemChange;  // a negative cost
                 tsum += c;
             }
             int64_t x = tsum;  // inclusive scan over the wave
@@ -174,8 +195,10 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             }
             if (lane == 63)
                 wave_tot[wave] = x;
-            if (tid == 0)
+            if (tid == 0) {
                 first[0] = -1;
+                first[3] = total_steps;  // vhi at the end of the last item
+            }
             __syncthreads();
             int64_t p = x - tsum, total = 0;
             for (int w = 0; w < NW; ++w) {
@@ -184,16 +207,27 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             }
             for (int i = i0; i < i1; ++i) {
                 const int64_t c = cost_of(i);
-                if (p <= lo && lo < p + c) {
+                const int64_t start = p - (int64_t)i * kProbeItemChange;  // real prefix
+                if (p <= vlo && vlo < p + c) {
                     first[0] = i;
-                    first[1] = p;
+                    first[1] = start + max<int64_t>(0, vlo - p - kProbeItemChange);
+                    first[2] = start;
                 }
+                if (p <= vhi && vhi < p + c)
+                    first[3] = start + max<int64_t>(0, vhi - p - kProbeItemChange);
                 p += c;
             }
             const bool any_neg = __syncthreads_or(neg);
-            ok = ok && !any_neg && total == a.total_cost && first[0] >= 0;
+            ok = ok && !any_neg && total == vtotal && first[0] >= 0;
+            auto uniform = [](int64_t x) -> int64_t {
+                const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)x);
+                const uint32_t h = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+                return (int64_t)(((uint64_t)h << 32) | l);
+            };
             item = __builtin_amdgcn_readfirstlane((int)first[0]);
-            pre = first[1];
+            lo = uniform(first[1]);
+            pre = uniform(first[2]);
+            hi = uniform(first[3]);
         }
     }
 
@@ -302,12 +336,20 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
              ((int64_t)ka1 * a.tile < (int64_t)seq_len + a.tile);
         if (!ok)
             break;
-        const int s0 = (int)max<int64_t>(lo - pre, 0);
-        const int s1 = (int)min<int64_t>(hi - pre, cost);
-        pre += cost;
+        const int s0 = (int)max<int64_t>(lo - pre, 0);  // the share's steps
+        const int s1 = (int)min<int64_t>(hi - pre, spt * cost);  // of the item
+        pre += spt * cost;
         const int wr0 = r0 + sub * a.rows_per_wg;  // first row of this workgroup
         if (wr0 >= r1)
             continue;  // ragged q-tile: no rows here (uniform)
+        // keys past the workgroup's last row are masked for all its rows
+        const int wg_last = min(wr0 + a.rows_per_wg, r1) - 1;
+        const int key_begin = ka0 * a.tile + s0 * kProbeStep;
+        const int key_end = min(ka0 * a.tile + s1 * kProbeStep, wg_last + 1);
+        const int nsteps =
+            key_end > key_begin ? (key_end - key_begin + kProbeStep - 1) / kProbeStep : 0;
+        if (nsteps == 0)
+            continue;  // the share holds no keys of these rows (uniform)
 
         const int row_base = wr0 + (wave % wph) * 32;
         const int my_row = row_base + r_lane;
@@ -329,12 +371,6 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
             }
         }
 
-        // keys past the workgroup's last row are masked for all its rows
-        const int wg_last = min(wr0 + a.rows_per_wg, r1) - 1;
-        const int key_begin = (ka0 + s0) * a.tile;
-        const int key_end = min((ka0 + s1) * a.tile, wg_last + 1);
-        const int nsteps =
-            key_end > key_begin ? (key_end - key_begin + kProbeStep - 1) / kProbeStep : 0;
         const int key_max = seq_len - 1;
         const uint16_t *kbase = a.k + (seq_off * a.hkv + g) * (int64_t)D;
         const uint16_t *vbase = a.v + (seq_off * a.hkv + g) * (int64_t)D;
@@ -621,10 +657,10 @@ int probe_rows_per_wg(int group, int tile)
 }
 
 // Work split of the probe over the workgroups of one (kv head, row block).
-// Equal shares of the kept k-tiles, one workgroup each, as many as fill
-// every compute unit's resident workgroups once (two for workgroups of at
-// most four waves, whose registers and LDS leave room for two per CU, else
-// one), when the schedule's longest item is more than half a share: then one
+// Equal shares of the kept steps (with a charge per item change), one
+// workgroup each, as many as fill every compute unit's resident workgroups
+// once (two for workgroups of at most four waves, whose registers and LDS
+// leave room for two per CU, else one), when the schedule's longest item is more than half a share: then one
 // item per workgroup would leave the pass waiting on the longest q-tile (at
 // 2K tokens: 16 k-tiles against a mean of 8.5).  Otherwise one workgroup per
 // item, in schedule order (heaviest first): the workgroups running at a time

@@ -79,7 +79,7 @@ def test_probe_parity(cu, hq, hkv, d, tile, S, W, L):
 def test_probe_shares(cu, hq, hkv, d, tile, S, W, L):
     """Any number of equal shares (one slot: each workgroup walks every item;
     more slots than k-tiles: most shares empty) gives the oracle's sums; the
-    shares cut items at k-tile boundaries, so the sums differ only in fp64
+    shares cut items at 64-key step boundaries, so the sums differ only in fp64
     summation order between slot counts."""
     runs = {}
     try:
