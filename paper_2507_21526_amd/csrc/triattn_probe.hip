@@ -159,6 +159,7 @@ __global__ __launch_bounds__(NW * 64, NW == 4 ? 2 : 1) void probe_kernel(ProbeAr
     if (a.per_item) {
         item = slot;
         hi = (int64_t)spt * sched[kHdrWords + (int64_t)item * kItemWords + I_COST];
+        ok = ok && hi >= 0;  // a negative cost would skip the item's checks
     } else {
         const int64_t vtotal = total_steps + (int64_t)kProbeItemChange * a.n_items;
         const int64_t per = (vtotal + a.n_slots - 1) / a.n_slots;

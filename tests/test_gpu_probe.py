@@ -115,6 +115,26 @@ def test_probe_corrupt_schedule_gives_nan():
         log(f"corrupt probe schedule ({what}): NaN sums")
 
 
+def test_probe_per_item_negative_cost_gives_nan():
+    """The per-item launch rejects a negative item cost, which would skip the
+    item's checks.  32K tokens, 8 heads of group 1: 256 q-tiles of at most
+    256 k-tiles against 64 slots of four-wave workgroups (2 per CU, 8 kv
+    heads), and 256 * 64 * 2 <= 256 * 257 / 2 kept k-tiles, so one workgroup
+    runs each item."""
+    cu, hq, hkv, d = [0, 32768], 8, 8, 128
+    q, k, v = (t.cuda() for t in draw_qkv(cu, hq, hkv, d, 9))
+    dout = draw_dout(cu, hq, d, 10).cuda()
+    lse = torch.zeros((hq, cu[-1]), dtype=torch.float32, device="cuda")
+    plan = B.Plan("causal", cu, 0, 1, 0, 128, hq, d, device="cuda")
+    assert plan.info.max_item_tiles * 64 * 2 <= plan.info.kept_tiles_per_qhead
+    got, _ = _probe(q, k, v, dout, lse, cu, 128, 16, 64, 32, 0.1, plan)
+    assert np.all(np.isfinite(got))
+    item = B.HDR_WORDS + B.ITEM_WORDS * (plan.info.n_items - 1)
+    plan.sched[item + 10] = -1
+    got, _ = _probe(q, k, v, dout, lse, cu, 128, 16, 64, 32, 0.1, plan)
+    assert np.isnan(got).any()
+
+
 def test_probe_paper_shape():
     # one Llama-3.1-8B layer on a 2K-token prompt with the probe's sections
     # (si 64, sl 128, last 128)
